@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark of the emulated batched SGEMM on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+                    [--flow F --ec E --tile T] [--no-cpu-baseline]
+
+A step is one sgemm_emu_batched call over the whole batch of the workload
+(every row of the hot path: global->LDS staging, split, three MFMA
+products, combine and store), with inputs already resident in HBM.  The
+default workload is the batched one, 4096 products of 128 x 128 x 128
+(uniform(-1, 1) FP32, seed 2).
+
+One JSON line is printed with the emulated TFLOP/s, the roofline of the
+dominant kernel (its average duration from HIP events recorded on the stream
+the kernel is launched on) and, as a reported baseline, the oracle's plain
+FP32 product timed on the host cores for a bounded sample of the same
+workload; the accuracy of the GPU result on that sample is reported with it.
+
+``--copy-calibration`` instead runs a plain device copy of known size, used
+to scale the HBM traffic counters of a profiler run.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import torch  # noqa: E402
+
+import paper_2308_15152_amd as pkg  # noqa: E402
+import synth  # noqa: E402
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_FP16_MFMA_TFLOPS = 2516.6   # dense
+PEAK_FP32_VECTOR_TFLOPS = 157.3
+
+METRIC = "emulated-SGEMM TFLOP/s (batched)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gemm_128", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--flow", type=int, default=pkg.FLOW_AUTO)
+    ap.add_argument("--ec", type=int, default=1)
+    ap.add_argument("--tile", type=int, default=pkg.TILE_AUTO)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target host time of the CPU-baseline sample")
+    ap.add_argument("--copy-calibration", action="store_true")
+    return ap.parse_args()
+
+
+def copy_calibration(steps: int):
+    """Plain device-to-device copy of 1 GiB, for counter calibration."""
+    n = 1 << 28
+    x = torch.rand(n, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "steps": steps,
+                      "ms_per_copy": dt * 1e3, "GBps": 8 * n / dt / 1e9}), flush=True)
+
+
+def make_call(w, inputs, policy):
+    if w.kind == "householder":
+        u, B = inputs
+        C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
+
+        def call():
+            pkg.householder_emu_batched(u, B, C)
+        return call, C
+    A, B = inputs
+    C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
+
+    def call():
+        pkg.sgemm_emu_batched(A, B, C, policy=policy)
+    return call, C
+
+
+def cpu_baseline(w, host_inputs, C_dev, target_s: float):
+    """The oracle's plain FP32 product on a bounded sample of the workload,
+    timed on the host cores; the same sample gives the accuracy of the GPU
+    result against the FP64 product."""
+    import numpy as np
+
+    import oracle
+
+    threads = oracle.num_threads()
+    if w.kind == "householder":
+        u, B = host_inputs
+        un, Bn = u.numpy(), B.numpy()
+
+        def run(items):
+            return oracle.householder(un, Bn, items=items, want=("c32",))
+
+        def ref(items):
+            return oracle.householder(un, Bn, items=items, want=("c64", "n64", "c32"))
+    else:
+        A, B = host_inputs
+
+        def run(items):
+            return oracle.gemm(A[items].numpy(), B[items].numpy(), want=("c32",))
+
+        def ref(items):
+            return oracle.gemm(A[items].numpy(), B[items].numpy(), want=("c64", "n64", "c32"))
+
+    per_item = 2.0 * w.m * w.n * w.k
+    if w.batch == 1:
+        # one huge product: sample whole output rows instead of items
+        A, B = host_inputs
+        rows = 8
+        t0 = time.perf_counter()
+        oracle.gemm(A[0, :rows].numpy()[None], B[0].numpy()[None], want=("c32",))
+        dt = time.perf_counter() - t0
+        est = max(1, int(rows * target_s / max(dt, 1e-3)))
+        rows = min(w.m, est)
+        t0 = time.perf_counter()
+        oracle.gemm(A[0, :rows].numpy()[None], B[0].numpy()[None], want=("c32",))
+        dt = time.perf_counter() - t0
+        flops = 2.0 * rows * w.n * w.k
+        g = np.random.default_rng(0)
+        ri = g.integers(0, w.m, 256)
+        ci = g.integers(0, w.n, 256)
+        r = oracle.dots(A[0].numpy()[ri], np.ascontiguousarray(B[0].numpy()[:, ci].T),
+                        want=("c64", "n64", "c32"))
+        Cs = C_dev[0].cpu().numpy()[ri, ci]
+        acc = {"max_rel_err_emu": oracle.max_rel_err(Cs, r["c64"], r["n64"]),
+               "max_rel_err_fp32": oracle.max_rel_err(r["c32"], r["c64"], r["n64"]),
+               "sample": "256 random elements"}
+        sample = f"{rows} of {w.m} output rows of the {w.m}x{w.n}x{w.k} product"
+        return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+                "kind": "oracle", "sample": sample, "seconds": dt}, acc
+
+    n = 1
+    t0 = time.perf_counter()
+    run([0])
+    dt1 = time.perf_counter() - t0
+    n = int(min(w.batch, max(threads, target_s / max(dt1, 1e-4))))
+    items = list(range(n))
+    t0 = time.perf_counter()
+    run(items)
+    dt = time.perf_counter() - t0
+    acc_items = items[:min(n, 16)]
+    r = ref(acc_items)
+    Cs = C_dev[acc_items].cpu().numpy()
+    acc = {"max_rel_err_emu": oracle.max_rel_err(Cs, r["c64"], r["n64"]),
+           "max_rel_err_fp32": oracle.max_rel_err(r["c32"], r["c64"], r["n64"]),
+           "sample": f"items 0..{len(acc_items) - 1}"}
+    sample = f"{n} of {w.batch} batch items"
+    return {"value": per_item * n / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle", "sample": sample, "seconds": dt}, acc
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the emulated SGEMM is a single-GPU "
+              "library (batch sharding across GPUs needs no communication and is not "
+              "part of this build)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    pkg.load()
+    if args.copy_calibration:
+        copy_calibration(args.steps)
+        return
+
+    w = synth.WORKLOADS[args.workload]
+    host_inputs = synth.workload_inputs(w)
+    dev_inputs = tuple(t.to("cuda") for t in host_inputs)
+    policy = None
+    if (args.flow, args.ec, args.tile) != (pkg.FLOW_AUTO, 1, pkg.TILE_AUTO):
+        policy = pkg.Policy(args.flow, args.ec, args.tile)
+    call, C = make_call(w, dev_inputs, policy)
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        call()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_events = ev0.elapsed_time(ev1)
+    ms_step = ms_events / args.steps
+
+    flops = w.flops
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    # dominant (and only) kernel: one launch per step
+    bytes_alg = w.algorithmic_bytes
+    if w.kind == "gemm" and w.batch == 1:
+        roof = {"bound": "mfma", "achieved": 3 * flops / (ms_step * 1e-3) / 1e12,
+                "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": bytes_alg / (ms_step * 1e-3) / 1e9,
+                "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = ("householder64_kernel" if w.kind == "householder" else "bgemm_emu_kernel")
+
+    out = {
+        "metric": METRIC,
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp16x3-mfma-fp32acc",
+        "data": "synthetic",
+        "config": {"workload": w.name, "kind": w.kind, "batch": w.batch, "m": w.m, "n": w.n,
+                   "k": w.k, "dist": w.dist, "seed": w.seed,
+                   "policy": None if policy is None else
+                   {"flow": policy.flow, "ec": policy.ec, "tile": policy.tile}},
+        "frac_fp32_vector_peak": tflops / PEAK_FP32_VECTOR_TFLOPS,
+        "frac_fp16_mfma_over_3": tflops / (PEAK_FP16_MFMA_TFLOPS / 3),
+        "hbm_GBps_algorithmic": bytes_alg / (ms_step * 1e-3) / 1e9,
+        "wall_s_timed": wall,
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        cb, acc = cpu_baseline(w, host_inputs, C, args.cpu_seconds)
+        out["cpu_baseline"] = cb
+        out["accuracy"] = acc
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

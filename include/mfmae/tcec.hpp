@@ -1,0 +1,129 @@
+// mfmae/tcec.hpp -- single-precision emulation on fp16 matrix instructions
+// with error correction (Sec. 4.4, eqs. corr-1..corr-5).
+//
+// An FP32 value x is split in registers into
+//     hi = toFP16(x),   lo = toFP16((x - toFP32(hi)) * 2^11)
+// (round to nearest even).  For |x| <= 65504 the subtraction and the scaling
+// are exact, so the split has exactly two roundings and is bit-reproducible.
+// The product of two split operands is then
+//     C = hiA.hiB + (loA.hiB + hiA.loB) / 2^11
+// where the term loA.loB is dropped (it is at most 2^-22 |a||b|).  The first
+// product goes to one FP32 accumulator and both correction products to a
+// second one, so the small correction terms are not rounded away against the
+// large main sum; the two are combined once, at the end, with one fused
+// multiply-add (the 2^-11 scaling is exact).
+//
+// The fragments are built straight from FP32 values held in registers; no
+// fp16 copy of the operands is ever written to memory by these functions.
+#pragma once
+
+#include "frag.hpp"
+
+namespace mfmae {
+namespace tcec {
+
+constexpr float kLoScale = 2048.0f;            // 2^11
+constexpr float kLoScaleInv = 1.0f / 2048.0f;  // 2^-11, exact
+
+// Split one value.
+__device__ inline void split(float x, _Float16& hi, _Float16& lo) {
+    hi = static_cast<_Float16>(x);
+    lo = static_cast<_Float16>((x - static_cast<float>(hi)) * kLoScale);
+}
+
+// Split two values into packed (low half = first value) hi and lo words.
+__device__ inline void split2(float x0, float x1, uint32_t& hi2, uint32_t& lo2) {
+    _Float16 h0, h1, l0, l1;
+    split(x0, h0, l0);
+    split(x1, h1, l1);
+    hi2 = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
+          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
+    lo2 = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
+          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
+}
+
+// Split eight consecutive values into one hi and one lo operand vector.
+__device__ inline void split8(const float (&x)[8], half8_t& hi, half8_t& lo) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        _Float16 h, l;
+        split(x[e], h, l);
+        hi[e] = h;
+        lo[e] = l;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fragment-level interface: the same shape of use as the plain fragments
+// (fill / build from a rule / mma / read back), with FP32 semantics.
+// ---------------------------------------------------------------------------
+
+template <class S, Use U>
+struct frag_emu {
+    half8_t hi, lo;
+};
+
+template <class S>
+struct acc_vec;
+template <>
+struct acc_vec<Shape16> {
+    using type = f32x4_t;
+};
+template <>
+struct acc_vec<Shape32> {
+    using type = f32x16_t;
+};
+
+template <class S>
+struct acc_emu {
+    using vec = typename acc_vec<S>::type;
+    static constexpr int num_elements = layout<S, Use::Acc>::num_elements;
+    vec main;  // sum of hi.hi
+    vec corr;  // sum of lo.hi + hi.lo, in units of 2^-11
+};
+
+template <class S>
+__device__ inline void fill_zero(acc_emu<S>& d) {
+#pragma unroll
+    for (int e = 0; e < acc_emu<S>::num_elements; ++e) {
+        d.main[e] = 0.0f;
+        d.corr[e] = 0.0f;
+    }
+}
+
+// Build an operand fragment from a rule: value(i, j) returns the FP32 entry
+// at matrix position (i, j); it is split in registers (foreach_ij over the
+// operand map, Sec. 4.2, applied to the FP32 emulation of Sec. 4.4).
+template <class S, Use U, class Fn>
+__device__ inline void build(frag_emu<S, U>& f, Fn&& value) {
+    using L = layout<S, U>;
+    const int l = lane_id();
+#pragma unroll
+    for (int e = 0; e < L::num_elements; ++e) {
+        _Float16 h, lo;
+        split(value(L::row(l, e), L::col(l, e)), h, lo);
+        f.hi[e] = h;
+        f.lo[e] = lo;
+    }
+}
+
+// d += a . b with error correction (3 MFMAs) or without (1 MFMA).
+template <bool EC, class S>
+__device__ inline void mma(acc_emu<S>& d, const frag_emu<S, Use::A>& a,
+                           const frag_emu<S, Use::B>& b) {
+    d.main = mfmae::mma(S{}, a.hi, b.hi, d.main);
+    if constexpr (EC) {
+        d.corr = mfmae::mma(S{}, a.lo, b.hi, d.corr);
+        d.corr = mfmae::mma(S{}, a.hi, b.lo, d.corr);
+    }
+}
+
+// The FP32 result of element e of this lane: main + corr * 2^-11, one
+// rounding.
+template <class S>
+__device__ inline float result(const acc_emu<S>& d, int e) {
+    return __builtin_fmaf(d.corr[e], kLoScaleInv, d.main[e]);
+}
+
+}  // namespace tcec
+}  // namespace mfmae

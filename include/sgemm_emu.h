@@ -1,0 +1,198 @@
+/*
+ * sgemm_emu.h -- C ABI of the single-precision-emulating GEMM library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method (Ootomo & Yokota, "Reducing shared memory footprint to leverage high
+ * throughput on Tensor Cores and its flexible API extension library",
+ * Sec. 4.4): every FP32 operand element x is split into two fp16 values
+ *     hi = toFP16(x),   lo = toFP16((x - toFP32(hi)) * 2^11)
+ * (round to nearest even), and the product is formed from three fp16 matrix
+ * products with FP32 accumulation,
+ *     C = hiA.hiB + (loA.hiB + hiA.loB) / 2^11      (eq. corr-5),
+ * with the two correction products accumulated apart from the main one.  The
+ * split is done in registers, so no fp16 copy of A or B is ever written to
+ * device memory or kept in LDS in addition to the FP32 data.
+ *
+ * Conventions shared by all entry points:
+ *   - Matrices are row-major FP32; "ld" is the distance in elements between
+ *     the starts of consecutive rows.
+ *   - Matrix pointers are DEVICE pointers owned by the caller.  The library
+ *     allocates no device memory and keeps no pointer after returning.
+ *   - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *     without waiting; buffers must stay valid until the stream reaches it.
+ *   - Inputs are expected to satisfy |x| <= 65504 (the fp16 range of hi);
+ *     outside that range, or for NaN/Inf, the result is unspecified.
+ *   - Every argument is validated before anything is enqueued.  On an error
+ *     nothing is launched and a negative code is returned; the functions
+ *     never throw and never abort.
+ *   - All functions are thread-safe: the library has no mutable global state
+ *     except the last HIP error code, which is kept per thread.
+ */
+#ifndef SGEMM_EMU_H
+#define SGEMM_EMU_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- Status codes ------------------------------------------------------ */
+#define SGEMM_EMU_OK 0
+#define SGEMM_EMU_ERR_DIM (-1)         /* negative m, n, k, batch or ncols    */
+#define SGEMM_EMU_ERR_LD (-2)          /* leading dimension too small          */
+#define SGEMM_EMU_ERR_NULL (-3)        /* NULL pointer with nonzero work       */
+#define SGEMM_EMU_ERR_STRIDE (-4)      /* negative stride, or C items overlap  */
+#define SGEMM_EMU_ERR_ALIAS (-5)       /* C overlaps A or B (or u)             */
+#define SGEMM_EMU_ERR_UNSUPPORTED (-6) /* size outside what an entry supports  */
+#define SGEMM_EMU_ERR_HIP (-7)         /* the HIP runtime reported an error    */
+#define SGEMM_EMU_ERR_POLICY (-8)      /* unknown policy value                 */
+
+/* Element strides between consecutive batch items of A, B and C.  A zero
+ * stride for A or B reuses (broadcasts) one matrix for every item; C's stride
+ * must keep items apart (stride.c >= (m-1)*ldc + n when batch > 1). */
+typedef struct {
+    int64_t a, b, c;
+} sgemm_emu_stride_t;
+
+/*
+ * Batched emulated SGEMM (Sec. 4.4; batched form of Sec. 4.4.2):
+ *   for t in [0, batch):  C_t := A_t . B_t
+ * with A_t = A + t*stride.a (m x k, row-major, lda >= max(1, k)),
+ *      B_t = B + t*stride.b (k x n, row-major, ldb >= max(1, n)),
+ *      C_t = C + t*stride.c (m x n, row-major, ldc >= max(1, n)).
+ * C is overwritten (no alpha/beta).  m = 0, n = 0 or batch = 0 is a no-op;
+ * k = 0 stores zeros.  Pointers need no particular alignment; 16-byte aligned
+ * bases with ld and strides multiples of 4 take the vector-load path.
+ * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL, _STRIDE, _ALIAS, _HIP.
+ */
+int sgemm_emu_batched(int m, int n, int k,
+                      const float* A, int lda,
+                      const float* B, int ldb,
+                      float* C, int ldc,
+                      int batch, sgemm_emu_stride_t stride,
+                      hipStream_t stream);
+
+/* Policy of the emulated product, after the paper's policy-based design
+ * (Sec. 4.4): the instruction shape and tiling, whether error correction is
+ * applied, and where the split happens.
+ *
+ * flow:
+ *   SGEMM_EMU_FLOW_AUTO   library choice (currently SPLIT for every shape).
+ *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
+ *                         global load and the LDS store; LDS holds hi and lo
+ *                         (the same 4 bytes per element as FP32) and the
+ *                         waves read ready operand vectors.
+ *   SGEMM_EMU_FLOW_DIRECT FP32 tiles in LDS; every wave reads FP32 and
+ *                         splits its own fragments in registers (the data
+ *                         flow of the paper's extension library, Fig. 6
+ *                         bottom).
+ *   SGEMM_EMU_FLOW_STAGED FP32 tiles in LDS; every wave converts its part to
+ *                         hi/lo, writes them back to LDS and reloads them as
+ *                         fragments (the flow forced by a load-only fragment
+ *                         API, Fig. 6 top).  Measurement only: three LDS
+ *                         passes per element instead of one.
+ * ec:   1 = error correction (3 products), 0 = hi.hi only (accuracy control).
+ * tile: 0 = automatic, or one of SGEMM_EMU_TILE_*.
+ */
+#define SGEMM_EMU_FLOW_AUTO 0
+#define SGEMM_EMU_FLOW_SPLIT 1
+#define SGEMM_EMU_FLOW_DIRECT 2
+#define SGEMM_EMU_FLOW_STAGED 3
+
+#define SGEMM_EMU_TILE_AUTO 0
+#define SGEMM_EMU_TILE_64x64 1   /* 4 waves of 32x32, k-chunk 32   */
+#define SGEMM_EMU_TILE_128x128 2 /* 4 waves of 64x64, k-chunk 32   */
+#define SGEMM_EMU_TILE_256x128 3 /* 8 waves of 64x64, k-chunk 32   */
+
+typedef struct {
+    int flow;
+    int ec;
+    int tile;
+} sgemm_emu_policy_t;
+
+/* sgemm_emu_batched with an explicit policy (NULL = automatic, with error
+ * correction).  Extra error: SGEMM_EMU_ERR_POLICY. */
+int sgemm_emu_batched_ex(int m, int n, int k,
+                         const float* A, int lda,
+                         const float* B, int ldb,
+                         float* C, int ldc,
+                         int batch, sgemm_emu_stride_t stride,
+                         const sgemm_emu_policy_t* policy,
+                         hipStream_t stream);
+
+/*
+ * Batched Householder application with the reflector built in registers
+ * (Sec. 4.2.1, eq. householder, read as H = I - 2 u u^T):
+ *   for t in [0, batch):  C_t := (I - 2 u_t u_t^T) . B_t
+ * u_t = u + t*stride_u (n FP32 values), B_t = B + t*stride_b (n x ncols,
+ * row-major, ldb >= max(1, ncols)), C_t = C + t*stride_c (n x ncols, ldc >=
+ * max(1, ncols)).  Each entry of H is formed as fmaf(-2 u_i, u_j, delta_ij)
+ * directly in the operand registers and then split as above; H is never
+ * stored.  u is used as given (it is not normalised).
+ * Supported: n == 64 and ldb < 2^27 (else SGEMM_EMU_ERR_UNSUPPORTED).
+ * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL, _STRIDE, _ALIAS, _UNSUPPORTED, _HIP.
+ */
+int householder_emu_batched(int n, const float* u, int64_t stride_u,
+                            const float* B, int ldb, int64_t stride_b, int ncols,
+                            float* C, int ldc, int64_t stride_c,
+                            int batch, hipStream_t stream);
+
+/*
+ * The split of Sec. 4.4 (eqs. corr-1/corr-2) applied elementwise on the
+ * device: hi[i], lo[i] receive the binary16 bit patterns of
+ * toFP16(x[i]) and toFP16((x[i] - toFP32(hi)) * 2^11).  count >= 0; x, hi
+ * and lo are device pointers of count elements and must not overlap.
+ * Errors: SGEMM_EMU_ERR_DIM, _NULL, _ALIAS, _HIP.
+ */
+int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+                    hipStream_t stream);
+
+/* ---- Fragment maps (Sec. 2.3.2, 4.2, 4.3) ------------------------------
+ * shape: MFMAE_SHAPE_16x16x32 (v_mfma_f32_16x16x32_f16) or
+ *        MFMAE_SHAPE_32x32x16 (v_mfma_f32_32x32x16_f16)
+ * use:   MFMAE_USE_A (M x K), MFMAE_USE_B (K x N), MFMAE_USE_ACC (M x N)
+ * Host-only table queries: no HIP call is made. */
+#define MFMAE_SHAPE_16x16x32 0
+#define MFMAE_SHAPE_32x32x16 1
+#define MFMAE_USE_A 0
+#define MFMAE_USE_B 1
+#define MFMAE_USE_ACC 2
+
+/* Elements per lane for (shape, use), or SGEMM_EMU_ERR_UNSUPPORTED. */
+int mfmae_num_elements(int shape, int use);
+
+/* Matrix position (i, j) -> lane (0..63) and element index holding it
+ * (the paper's `map`, Sec. 4.3).  Errors: _UNSUPPORTED, _DIM (out of range),
+ * _NULL. */
+int mfmae_map(int shape, int use, int i, int j, int* lane, int* elem);
+
+/* For one lane, the matrix position of each of its elements (the index part
+ * of the paper's `foreach_ij`, Sec. 4.2): i_out[e], j_out[e] for
+ * e < mfmae_num_elements(shape, use).  Errors: _UNSUPPORTED, _DIM, _NULL. */
+int mfmae_foreach(int shape, int use, int lane, int* i_out, int* j_out);
+
+/* Run ONE fp16 MFMA of the given shape on one wavefront with operands given
+ * lane by lane (the register-level counterpart of the paper's mapping probe,
+ * Sec. 2.3.2): a[lane*8 + e], b[lane*8 + e] are binary16 bit patterns of
+ * element e of that lane's A and B operand, the accumulator starts at zero,
+ * and d[lane*n + e] receives element e of the lane's result (n = 4 for
+ * 16x16x32, 16 for 32x32x16).  Device pointers.
+ * Errors: _UNSUPPORTED, _NULL, _HIP. */
+int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
+                    hipStream_t stream);
+
+/* ---- Diagnostics ------------------------------------------------------- */
+/* Static text for a status code. */
+const char* sgemm_emu_strerror(int code);
+/* The hipError_t behind the calling thread's last SGEMM_EMU_ERR_HIP (0 if
+ * none). */
+int sgemm_emu_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGEMM_EMU_H */

@@ -48,6 +48,8 @@ def _load():
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int, ctypes.c_int64
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_f32_to_f16.argtypes = [ctypes.c_float]
     lib.oracle_f32_to_f16.restype = ctypes.c_uint16
     lib.oracle_f16_to_f32.argtypes = [ctypes.c_uint16]
@@ -68,6 +70,11 @@ def _load():
     lib.oracle_householder.restype = None
     _lib = lib
     return lib
+
+
+def num_threads() -> int:
+    """Threads the oracle's parallel loops use."""
+    return int(_load().oracle_num_threads())
 
 
 def _ptr(a):

@@ -1,0 +1,270 @@
+"""Single-precision-emulating batched GEMM on MI355X (gfx950) matrix cores.
+
+Python binding of ``libsgemm_emu.so`` (C ABI in ``include/sgemm_emu.h``).
+Every function here only marshals arguments: sizes, strides and device
+pointers are read off torch tensors and handed to the C entry point of the
+same name, on the current torch stream.  All arithmetic runs in the HIP
+kernels; there is no fallback path, and a missing library is an error.
+
+Method (Ootomo & Yokota, HPC Asia 2023, Sec. 4.4): each FP32 operand is
+split in registers into fp16 hi and lo = fp16((x - hi) * 2^11); three fp16
+MFMA products hi.hi, lo.hi and hi.lo are accumulated in FP32, the two
+correction products in their own accumulator, and C = main + corr * 2^-11.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "SgemmEmuError", "lib_path", "load",
+    "sgemm_emu_batched", "sgemm_emu_batched_ex", "householder_emu_batched",
+    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
+    "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+    "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED",
+    "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128",
+    "SHAPE_16x16x32", "SHAPE_32x32x16", "USE_A", "USE_B", "USE_ACC",
+    "EXPORTED_SYMBOLS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_NAME = "libsgemm_emu.so"
+
+FLOW_AUTO, FLOW_SPLIT, FLOW_DIRECT, FLOW_STAGED = 0, 1, 2, 3
+TILE_AUTO, TILE_64x64, TILE_128x128, TILE_256x128 = 0, 1, 2, 3
+SHAPE_16x16x32, SHAPE_32x32x16 = 0, 1
+USE_A, USE_B, USE_ACC = 0, 1, 2
+
+# Every symbol declared in include/sgemm_emu.h.
+EXPORTED_SYMBOLS = (
+    "sgemm_emu_batched", "sgemm_emu_batched_ex", "householder_emu_batched",
+    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
+    "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+)
+
+
+class SgemmEmuError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        msg = _strerror(code)
+        if code == -7:
+            msg += f" (hipError {sgemm_emu_last_hip_error()})"
+        super().__init__(f"{where}: {msg} [code {code}]")
+        self.code = code
+
+
+class Stride(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_int64), ("b", ctypes.c_int64), ("c", ctypes.c_int64)]
+
+
+class Policy(ctypes.Structure):
+    """Policy of the emulated product (flow, error correction, tile)."""
+    _fields_ = [("flow", ctypes.c_int), ("ec", ctypes.c_int), ("tile", ctypes.c_int)]
+
+    def __init__(self, flow: int = FLOW_AUTO, ec: int = 1, tile: int = TILE_AUTO):
+        super().__init__(flow, ec, tile)
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return os.environ.get("SGEMM_EMU_LIB", os.path.join(_HERE, LIB_NAME))
+
+
+def load():
+    """Load the shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = lib_path()
+    if not os.path.exists(path):
+        raise ImportError(
+            f"{path} not found: build it first (python -c 'import __graft_entry__ as g; g.build()'"
+            " or python paper_2308_15152_amd/build.py)")
+    lib = ctypes.CDLL(path)
+    i32, i64, P = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+    ip = ctypes.POINTER(ctypes.c_int)
+    sig = {
+        "sgemm_emu_batched": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride, P], i32),
+        "sgemm_emu_batched_ex": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
+                                  ctypes.POINTER(Policy), P], i32),
+        "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
+        "sgemm_emu_split": ([i64, P, P, P, P], i32),
+        "mfmae_num_elements": ([i32, i32], i32),
+        "mfmae_map": ([i32, i32, i32, i32, ip, ip], i32),
+        "mfmae_foreach": ([i32, i32, i32, ip, ip], i32),
+        "mfmae_mma_probe": ([i32, P, P, P, P], i32),
+        "sgemm_emu_strerror": ([i32], ctypes.c_char_p),
+        "sgemm_emu_last_hip_error": ([], i32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _strerror(code: int) -> str:
+    return load().sgemm_emu_strerror(int(code)).decode()
+
+
+def sgemm_emu_strerror(code: int) -> str:
+    return _strerror(code)
+
+
+def sgemm_emu_last_hip_error() -> int:
+    return int(load().sgemm_emu_last_hip_error())
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != 0:
+        raise SgemmEmuError(rc, where)
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(stream))
+    import torch
+
+    if torch.cuda.is_available() and torch.cuda.is_initialized():
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    return ctypes.c_void_p(0)
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    return ctypes.c_void_p(0 if t is None else int(t.data_ptr()))
+
+
+def _matrix_view(t, name: str):
+    """(batch, rows, cols, ld, batch_stride) of a 2-D or 3-D FP32 tensor whose
+    rows are contiguous."""
+    import torch
+
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dim() == 2:
+        rows, cols = t.shape
+        if cols > 1 and t.stride(1) != 1:
+            raise ValueError(f"{name} rows must be contiguous (stride 1 along the last dim)")
+        return None, rows, cols, t.stride(0) if rows > 1 else max(cols, 1), 0
+    if t.dim() != 3:
+        raise ValueError(f"{name} must be 2-D or 3-D")
+    b, rows, cols = t.shape
+    if cols > 1 and t.stride(2) != 1:
+        raise ValueError(f"{name} rows must be contiguous (stride 1 along the last dim)")
+    ld = t.stride(1) if rows > 1 else max(cols, 1)
+    return b, rows, cols, ld, t.stride(0) if b > 1 else 0
+
+
+def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None):
+    """C[t] := A[t] @ B[t] with the emulated FP32 product.
+
+    A: [batch, m, k] or [m, k]; B: [batch, k, n] or [k, n] (a 2-D operand is
+    broadcast over the batch); C: [batch, m, n] (allocated if None).  Rows of
+    every operand must be contiguous; leading dimensions and batch strides are
+    taken from the tensors' strides.  Runs on the current torch stream unless
+    ``stream`` (a hipStream_t handle) is given.  With ``policy`` the call goes
+    to sgemm_emu_batched_ex."""
+    import torch
+
+    ba, m, k, lda, sa = _matrix_view(A, "A")
+    bb, kb, n, ldb, sb = _matrix_view(B, "B")
+    if kb != k:
+        raise ValueError(f"inner dimensions differ: A is {m}x{k}, B is {kb}x{n}")
+    batch = ba if ba is not None else (bb if bb is not None else 1)
+    if ba is not None and bb is not None and ba != bb:
+        raise ValueError("batch sizes differ")
+    if C is None:
+        C = torch.empty((batch, m, n), dtype=torch.float32, device=A.device)
+    bc, mc, nc, ldc, sc = _matrix_view(C if C.dim() == 3 else C.unsqueeze(0), "C")
+    if (mc, nc) != (m, n) or (bc or 1) != batch:
+        raise ValueError("C has the wrong shape")
+    st = Stride(sa, sb, sc if batch > 1 else 0)
+    lib = load()
+    if policy is None:
+        rc = lib.sgemm_emu_batched(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
+                                   st, _stream(stream))
+        _check(rc, "sgemm_emu_batched")
+    else:
+        rc = lib.sgemm_emu_batched_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
+                                      st, ctypes.byref(policy), _stream(stream))
+        _check(rc, "sgemm_emu_batched_ex")
+    return C
+
+
+def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):
+    return sgemm_emu_batched(A, B, C, policy=policy, stream=stream)
+
+
+def householder_emu_batched(u, B, C=None, *, stream=None):
+    """C[t] := (I - 2 u[t] u[t]^T) @ B[t]; u: [batch, 64], B: [batch, 64, ncols]."""
+    import torch
+
+    if u.dtype != torch.float32 or not u.is_cuda or u.dim() != 2:
+        raise ValueError("u must be a [batch, n] float32 device tensor")
+    batch, n = u.shape
+    if n > 1 and u.stride(1) != 1:
+        raise ValueError("u rows must be contiguous")
+    bb, nb, ncols, ldb, sb = _matrix_view(B, "B")
+    if nb != n or (bb or 1) != batch:
+        raise ValueError("B must be [batch, n, ncols]")
+    if C is None:
+        C = torch.empty((batch, n, ncols), dtype=torch.float32, device=u.device)
+    _, _, _, ldc, sc = _matrix_view(C, "C")
+    su = u.stride(0) if batch > 1 else 0
+    rc = load().householder_emu_batched(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C), ldc,
+                                        sc, batch, _stream(stream))
+    _check(rc, "householder_emu_batched")
+    return C
+
+
+def sgemm_emu_split(x, *, stream=None):
+    """Elementwise split on the device: (hi, lo) binary16 bit patterns as int16
+    tensors of x's shape (x: contiguous float32 device tensor)."""
+    import torch
+
+    if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous float32 device tensor")
+    hi = torch.empty(x.shape, dtype=torch.int16, device=x.device)
+    lo = torch.empty(x.shape, dtype=torch.int16, device=x.device)
+    rc = load().sgemm_emu_split(x.numel(), _ptr(x), _ptr(hi), _ptr(lo), _stream(stream))
+    _check(rc, "sgemm_emu_split")
+    return hi, lo
+
+
+def mfmae_num_elements(shape: int, use: int) -> int:
+    rc = int(load().mfmae_num_elements(shape, use))
+    _check(min(rc, 0), "mfmae_num_elements")
+    return rc
+
+
+def mfmae_map(shape: int, use: int, i: int, j: int):
+    """(lane, element) holding matrix position (i, j)."""
+    lane, elem = ctypes.c_int(), ctypes.c_int()
+    _check(load().mfmae_map(shape, use, i, j, ctypes.byref(lane), ctypes.byref(elem)), "mfmae_map")
+    return lane.value, elem.value
+
+
+def mfmae_foreach(shape: int, use: int, lane: int):
+    """[(i, j) for each element of `lane`]."""
+    n = mfmae_num_elements(shape, use)
+    ii = (ctypes.c_int * n)()
+    jj = (ctypes.c_int * n)()
+    _check(load().mfmae_foreach(shape, use, lane, ii, jj), "mfmae_foreach")
+    return list(zip(list(ii), list(jj)))
+
+
+def mfmae_mma_probe(shape: int, a_lanes, b_lanes, *, stream=None):
+    """One MFMA on operands given lane by lane: a_lanes, b_lanes are [64, 8]
+    int16 device tensors of binary16 bit patterns; returns the [64, n] FP32
+    accumulator (n = 4 or 16) with the accumulator starting at zero."""
+    import torch
+
+    n = mfmae_num_elements(shape, USE_ACC)
+    d = torch.empty((64, n), dtype=torch.float32, device=a_lanes.device)
+    rc = load().mfmae_mma_probe(shape, _ptr(a_lanes), _ptr(b_lanes), _ptr(d), _stream(stream))
+    _check(rc, "mfmae_mma_probe")
+    return d

@@ -1,0 +1,256 @@
+// C ABI of the library (declared in include/sgemm_emu.h): argument
+// validation, kernel choice and launch.  Validation runs entirely on the host
+// before any HIP call, so every error path is free of side effects.
+#include <stdint.h>
+
+#include "internal.h"
+#include "mfmae/frag.hpp"
+#include "sgemm_emu.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+int hip_fail(hipError_t e) {
+    g_last_hip_error = (int)e;
+    return SGEMM_EMU_ERR_HIP;
+}
+
+struct Extent {
+    uintptr_t lo, hi;  // [lo, hi) in bytes; empty if lo == hi
+};
+
+// Bytes spanned by `items` row-major matrices of rows x cols with leading
+// dimension ld and item stride s (elements), starting at p.
+Extent extent(const void* p, int64_t items, int64_t rows, int64_t cols, int64_t ld, int64_t s) {
+    Extent e{(uintptr_t)p, (uintptr_t)p};
+    if (items <= 0 || rows <= 0 || cols <= 0) return e;
+    const int64_t last = (items - 1) * s + (rows - 1) * ld + cols;  // elements
+    e.hi = e.lo + (uintptr_t)last * sizeof(float);
+    return e;
+}
+
+bool overlap(Extent a, Extent b) {
+    if (a.lo == a.hi || b.lo == b.hi) return false;
+    return a.lo < b.hi && b.lo < a.hi;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int pick_tile(int m, int n, int batch) {
+    if (m <= 64 && n <= 64) return SGEMM_EMU_TILE_64x64;
+    const int64_t big = (int64_t)((m + 255) / 256) * ((n + 127) / 128) * batch;
+    if (m >= 256 && big >= 1024) return SGEMM_EMU_TILE_256x128;
+    return SGEMM_EMU_TILE_128x128;
+}
+
+// Validation shared by the two GEMM entry points.
+int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
+               int ldc, int batch, sgemm_emu_stride_t st) {
+    if (m < 0 || n < 0 || k < 0 || batch < 0) return SGEMM_EMU_ERR_DIM;
+    if (lda < (k > 1 ? k : 1) || ldb < (n > 1 ? n : 1) || ldc < (n > 1 ? n : 1))
+        return SGEMM_EMU_ERR_LD;
+    if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
+    if (C == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (k > 0 && (A == nullptr || B == nullptr)) return SGEMM_EMU_ERR_NULL;
+    if (st.a < 0 || st.b < 0 || st.c < 0) return SGEMM_EMU_ERR_STRIDE;
+    if (batch > 1 && st.c < (int64_t)(m - 1) * ldc + n) return SGEMM_EMU_ERR_STRIDE;
+    const Extent ec = extent(C, batch, m, n, ldc, st.c);
+    if (k > 0) {
+        const Extent ea = extent(A, st.a == 0 ? 1 : batch, m, k, lda, st.a);
+        const Extent eb = extent(B, st.b == 0 ? 1 : batch, k, n, ldb, st.b);
+        if (overlap(ec, ea) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
+    }
+    return SGEMM_EMU_OK;
+}
+
+int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
+             int ldc, int batch, sgemm_emu_stride_t st, int flow, int ec, int tile,
+             hipStream_t stream) {
+    int rc = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st);
+    if (rc != SGEMM_EMU_OK) return rc;
+    if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_STAGED) return SGEMM_EMU_ERR_POLICY;
+    if (ec != 0 && ec != 1) return SGEMM_EMU_ERR_POLICY;
+    if (tile < SGEMM_EMU_TILE_AUTO || tile > SGEMM_EMU_TILE_256x128) return SGEMM_EMU_ERR_POLICY;
+    if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
+    if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
+    if (flow == SGEMM_EMU_FLOW_AUTO) flow = SGEMM_EMU_FLOW_SPLIT;
+    if (!sgemm_emu::gemm_variant_exists(tile, flow)) return SGEMM_EMU_ERR_POLICY;
+
+    sgemm_emu::GemmArgs a;
+    a.m = m;
+    a.n = n;
+    a.k = k;
+    a.A = A;
+    a.lda = lda;
+    a.sa = st.a;
+    a.B = B;
+    a.ldb = ldb;
+    a.sb = st.b;
+    a.C = C;
+    a.ldc = ldc;
+    a.sc = st.c;
+    a.batch = batch;
+    a.vec_a = aligned16(A) && lda % 4 == 0 && st.a % 4 == 0;
+    a.vec_b = aligned16(B) && ldb % 4 == 0 && st.b % 4 == 0;
+    hipError_t e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
+template <class S>
+int map_impl(int use, int i, int j, int* lane, int* elem) {
+    using namespace mfmae;
+    switch (use) {
+        case MFMAE_USE_A:
+            if (i < 0 || i >= S::M || j < 0 || j >= S::K) return SGEMM_EMU_ERR_DIM;
+            *lane = layout<S, Use::A>::lane_of(i, j);
+            *elem = layout<S, Use::A>::elem_of(i, j);
+            return SGEMM_EMU_OK;
+        case MFMAE_USE_B:
+            if (i < 0 || i >= S::K || j < 0 || j >= S::N) return SGEMM_EMU_ERR_DIM;
+            *lane = layout<S, Use::B>::lane_of(i, j);
+            *elem = layout<S, Use::B>::elem_of(i, j);
+            return SGEMM_EMU_OK;
+        case MFMAE_USE_ACC:
+            if (i < 0 || i >= S::M || j < 0 || j >= S::N) return SGEMM_EMU_ERR_DIM;
+            *lane = layout<S, Use::Acc>::lane_of(i, j);
+            *elem = layout<S, Use::Acc>::elem_of(i, j);
+            return SGEMM_EMU_OK;
+        default: return SGEMM_EMU_ERR_UNSUPPORTED;
+    }
+}
+
+template <class L>
+void foreach_fill(int lane, int* i_out, int* j_out) {
+    for (int e = 0; e < L::num_elements; ++e) {
+        i_out[e] = L::row(lane, e);
+        j_out[e] = L::col(lane, e);
+    }
+}
+
+template <class S>
+int foreach_impl(int use, int lane, int* i_out, int* j_out) {
+    using namespace mfmae;
+    switch (use) {
+        case MFMAE_USE_A: foreach_fill<layout<S, Use::A>>(lane, i_out, j_out); return SGEMM_EMU_OK;
+        case MFMAE_USE_B: foreach_fill<layout<S, Use::B>>(lane, i_out, j_out); return SGEMM_EMU_OK;
+        case MFMAE_USE_ACC:
+            foreach_fill<layout<S, Use::Acc>>(lane, i_out, j_out);
+            return SGEMM_EMU_OK;
+        default: return SGEMM_EMU_ERR_UNSUPPORTED;
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+int sgemm_emu_batched(int m, int n, int k, const float* A, int lda, const float* B, int ldb,
+                      float* C, int ldc, int batch, sgemm_emu_stride_t stride,
+                      hipStream_t stream) {
+    return run_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, SGEMM_EMU_FLOW_AUTO, 1,
+                    SGEMM_EMU_TILE_AUTO, stream);
+}
+
+int sgemm_emu_batched_ex(int m, int n, int k, const float* A, int lda, const float* B, int ldb,
+                         float* C, int ldc, int batch, sgemm_emu_stride_t stride,
+                         const sgemm_emu_policy_t* policy, hipStream_t stream) {
+    sgemm_emu_policy_t pol{SGEMM_EMU_FLOW_AUTO, 1, SGEMM_EMU_TILE_AUTO};
+    if (policy) pol = *policy;
+    return run_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, pol.flow, pol.ec, pol.tile,
+                    stream);
+}
+
+int householder_emu_batched(int n, const float* u, int64_t stride_u, const float* B, int ldb,
+                            int64_t stride_b, int ncols, float* C, int ldc, int64_t stride_c,
+                            int batch, hipStream_t stream) {
+    if (n < 0 || ncols < 0 || batch < 0) return SGEMM_EMU_ERR_DIM;
+    if (ldb < (ncols > 1 ? ncols : 1) || ldc < (ncols > 1 ? ncols : 1)) return SGEMM_EMU_ERR_LD;
+    if (n == 0 || ncols == 0 || batch == 0) return SGEMM_EMU_OK;
+    if (n != 64) return SGEMM_EMU_ERR_UNSUPPORTED;
+    // the kernel forms 8 * ldb + column as a 32-bit lane offset
+    if (ldb >= (1 << 27)) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (u == nullptr || B == nullptr || C == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (stride_u < 0 || stride_b < 0 || stride_c < 0) return SGEMM_EMU_ERR_STRIDE;
+    if (batch > 1 && stride_c < (int64_t)(n - 1) * ldc + ncols) return SGEMM_EMU_ERR_STRIDE;
+    const Extent ec = extent(C, batch, n, ncols, ldc, stride_c);
+    const Extent eu = extent(u, stride_u == 0 ? 1 : batch, 1, n, n, stride_u);
+    const Extent eb = extent(B, stride_b == 0 ? 1 : batch, n, ncols, ldb, stride_b);
+    if (overlap(ec, eu) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
+    sgemm_emu::HouseholderArgs a;
+    a.ncols = ncols;
+    a.u = u;
+    a.su = stride_u;
+    a.B = B;
+    a.ldb = ldb;
+    a.sb = stride_b;
+    a.C = C;
+    a.ldc = ldc;
+    a.sc = stride_c;
+    a.batch = batch;
+    hipError_t e = sgemm_emu::launch_householder64(a, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
+int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+                    hipStream_t stream) {
+    if (count < 0) return SGEMM_EMU_ERR_DIM;
+    if (count == 0) return SGEMM_EMU_OK;
+    if (x == nullptr || hi == nullptr || lo == nullptr) return SGEMM_EMU_ERR_NULL;
+    const Extent ex{(uintptr_t)x, (uintptr_t)x + (uintptr_t)count * 4};
+    const Extent eh{(uintptr_t)hi, (uintptr_t)hi + (uintptr_t)count * 2};
+    const Extent el{(uintptr_t)lo, (uintptr_t)lo + (uintptr_t)count * 2};
+    if (overlap(ex, eh) || overlap(ex, el) || overlap(eh, el)) return SGEMM_EMU_ERR_ALIAS;
+    hipError_t e = sgemm_emu::launch_split(count, x, hi, lo, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
+int mfmae_num_elements(int shape, int use) {
+    if (use < MFMAE_USE_A || use > MFMAE_USE_ACC) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (shape == MFMAE_SHAPE_16x16x32) return use == MFMAE_USE_ACC ? 4 : 8;
+    if (shape == MFMAE_SHAPE_32x32x16) return use == MFMAE_USE_ACC ? 16 : 8;
+    return SGEMM_EMU_ERR_UNSUPPORTED;
+}
+
+int mfmae_map(int shape, int use, int i, int j, int* lane, int* elem) {
+    if (lane == nullptr || elem == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (shape == MFMAE_SHAPE_16x16x32) return map_impl<mfmae::Shape16>(use, i, j, lane, elem);
+    if (shape == MFMAE_SHAPE_32x32x16) return map_impl<mfmae::Shape32>(use, i, j, lane, elem);
+    return SGEMM_EMU_ERR_UNSUPPORTED;
+}
+
+int mfmae_foreach(int shape, int use, int lane, int* i_out, int* j_out) {
+    if (mfmae_num_elements(shape, use) < 0) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (lane < 0 || lane >= 64) return SGEMM_EMU_ERR_DIM;
+    if (i_out == nullptr || j_out == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (shape == MFMAE_SHAPE_16x16x32) return foreach_impl<mfmae::Shape16>(use, lane, i_out, j_out);
+    return foreach_impl<mfmae::Shape32>(use, lane, i_out, j_out);
+}
+
+int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
+                    hipStream_t stream) {
+    if (shape != MFMAE_SHAPE_16x16x32 && shape != MFMAE_SHAPE_32x32x16)
+        return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (a == nullptr || b == nullptr || d == nullptr) return SGEMM_EMU_ERR_NULL;
+    hipError_t e = sgemm_emu::launch_mma_probe(shape, a, b, d, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
+const char* sgemm_emu_strerror(int code) {
+    switch (code) {
+        case SGEMM_EMU_OK: return "success";
+        case SGEMM_EMU_ERR_DIM: return "negative or out-of-range size";
+        case SGEMM_EMU_ERR_LD: return "leading dimension too small";
+        case SGEMM_EMU_ERR_NULL: return "null pointer with nonzero work";
+        case SGEMM_EMU_ERR_STRIDE: return "negative batch stride or overlapping output items";
+        case SGEMM_EMU_ERR_ALIAS: return "output overlaps an input";
+        case SGEMM_EMU_ERR_UNSUPPORTED: return "unsupported size or shape";
+        case SGEMM_EMU_ERR_HIP: return "HIP runtime error";
+        case SGEMM_EMU_ERR_POLICY: return "invalid or unavailable policy";
+        default: return "unknown status code";
+    }
+}
+
+int sgemm_emu_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

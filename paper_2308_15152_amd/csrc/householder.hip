@@ -1,0 +1,163 @@
+// Batched Householder application C = (I - 2 u u^T) B with the reflector
+// built directly in the MFMA A-operand registers (Sec. 4.2.1, eq. householder;
+// the rule-built fragment of Sec. 4.2), in emulated FP32 (Sec. 4.4).
+//
+// One wavefront handles one batch item (n = 64) and up to 64 columns of B.  H is never stored: each
+// lane evaluates, for every A-operand element it holds, h_ij =
+// fmaf(-2 u_i, u_j, delta_ij) and splits it into hi/lo in registers.  Per
+// 16-wide k step one foreach_ij over the A-operand map fills both 32-row
+// blocks of the reflector (the index computation is shared by the two
+// fragments, and -2 u_i of the lane's rows is computed once), which is what
+// keeps rule-built fragments cheaper than a trip through memory.
+//
+// B is read straight from global memory into the B-operand registers: lane l
+// holds column l % 32 of a 32-column block, so for a fixed k the 32 lanes of
+// a half-wave read one 128-byte row segment.  Neither H nor B goes through
+// LDS; the kernel is bound by HBM traffic (u, B read once, C written once).
+#include "internal.h"
+#include "mfmae/frag.hpp"
+#include "mfmae/tcec.hpp"
+
+namespace sgemm_emu {
+
+using mfmae::f32x16_t;
+using mfmae::half8_t;
+using mfmae::Shape32;
+using mfmae::Use;
+
+struct HhParams {
+    int ncols;
+    const float* u;
+    int64_t su;
+    const float* B;
+    int64_t ldb, sb;
+    float* C;
+    int64_t ldc, sc;
+    int batch;
+};
+
+constexpr int kHhWaves = 4;  // waves (tasks) per workgroup
+
+__global__ __launch_bounds__(64 * kHhWaves, 2) void householder64_kernel(HhParams p) {
+    // wave index as a wave-uniform (scalar) value, so that the per-item base
+    // pointers below live in SGPRs and loads use scalar-base addressing
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int l = threadIdx.x & 63;
+    // one wave per (item, group of 64 columns)
+    const int64_t task = (int64_t)blockIdx.x * kHhWaves + wave;
+    const int ngroups = (p.ncols + 63) / 64;
+    const int64_t item = task / ngroups;
+    const int c0 = (int)(task - item * ngroups) * 64;
+    if (item >= p.batch) return;  // whole wave; the kernel has no barrier
+
+    const float* __restrict__ u = p.u + item * p.su;
+    const float* __restrict__ Bi = p.B + item * p.sb;
+    float* __restrict__ Ci = p.C + item * p.sc;
+
+    using FragA = mfmae::fragment<Shape32, Use::A, _Float16>;
+
+    // Row of each of the two 32-row blocks of H this lane holds.
+    float urow[2];
+    mfmae::foreach_ij<FragA>([&](int e, int i, int) {
+        if (e == 0) {
+            urow[0] = -2.0f * u[i];
+            urow[1] = -2.0f * u[32 + i];
+        }
+    });
+
+    // This wave's 64 columns (two 32-column MFMA blocks).
+    {
+        f32x16_t acc[2][2], cor[2][2];
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    acc[tm][cb][e] = 0.0f;
+                    cor[tm][cb][e] = 0.0f;
+                }
+
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            // B operands of this 16-wide k step for both column blocks.  Lane l
+            // holds B[16 s + 8 (l / 32) + e][c0 + 32 cb + l % 32]; the row
+            // start of (s, e) is wave-uniform and the lane part is a 32-bit
+            // offset.
+            half8_t bh[2], bl[2];
+            const int lane_off = 8 * (l >> 5) * (int)p.ldb + (l & 31);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float* rowp = Bi + (int64_t)(16 * s + e) * p.ldb + c0;
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const bool ok = c0 + 32 * cb + (l & 31) < p.ncols;
+                    const float x = ok ? rowp[lane_off + 32 * cb] : 0.0f;
+                    _Float16 vh, vl;
+                    mfmae::tcec::split(x, vh, vl);
+                    bh[cb][e] = vh;
+                    bl[cb][e] = vl;
+                }
+            }
+            // Reflector operands of this k step for both row blocks, built
+            // from the rule h_ij = fmaf(-2 u_i, u_j, delta_ij).
+            half8_t hh[2], hl[2];
+            const float* us = u + 16 * s + 8 * (l >> 5);
+            mfmae::foreach_ij<FragA>([&](int e, int i, int j) {
+                const int gj = 16 * s + j;
+                const float uj = us[e];  // u[gj]: j = 8 (l / 32) + e
+#pragma unroll
+                for (int tm = 0; tm < 2; ++tm) {
+                    const float h = __builtin_fmaf(urow[tm], uj, (32 * tm + i) == gj ? 1.0f : 0.0f);
+                    _Float16 vh, vl;
+                    mfmae::tcec::split(h, vh, vl);
+                    hh[tm][e] = vh;
+                    hl[tm][e] = vl;
+                }
+            });
+#pragma unroll
+            for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    acc[tm][cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(hh[tm], bh[cb], acc[tm][cb], 0, 0, 0);
+                    cor[tm][cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(hl[tm], bh[cb], cor[tm][cb], 0, 0, 0);
+                    cor[tm][cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(hh[tm], bl[cb], cor[tm][cb], 0, 0, 0);
+                }
+        }
+
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            const int col = c0 + 32 * cb + (l & 31);
+            if (col >= p.ncols) continue;
+#pragma unroll
+            for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = 32 * tm + mfmae::layout<Shape32, Use::Acc>::row(l, e);
+                    Ci[(int64_t)row * p.ldc + col] =
+                        __builtin_fmaf(cor[tm][cb][e], mfmae::tcec::kLoScaleInv, acc[tm][cb][e]);
+                }
+        }
+    }
+}
+
+hipError_t launch_householder64(const HouseholderArgs& a, hipStream_t stream) {
+    HhParams p;
+    p.ncols = a.ncols;
+    p.u = a.u;
+    p.su = a.su;
+    p.B = a.B;
+    p.ldb = a.ldb;
+    p.sb = a.sb;
+    p.C = a.C;
+    p.ldc = a.ldc;
+    p.sc = a.sc;
+    p.batch = a.batch;
+    const int64_t tasks = (int64_t)a.batch * ((a.ncols + 63) / 64);
+    const int64_t blocks = (tasks + kHhWaves - 1) / kHhWaves;
+    hipLaunchKernelGGL(householder64_kernel, dim3((unsigned)blocks), dim3(64 * kHhWaves), 0,
+                       stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace sgemm_emu

@@ -1,0 +1,48 @@
+// Internal declarations shared by the C ABI and the kernel translation units.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace sgemm_emu {
+
+struct GemmArgs {
+    int m, n, k;
+    const float* A;
+    int64_t lda, sa;
+    const float* B;
+    int64_t ldb, sb;
+    float* C;
+    int64_t ldc, sc;
+    int batch;
+    bool vec_a, vec_b;  // 16-byte vector loads are legal for A / B
+};
+
+// Launch the batched emulated GEMM with the given tile / flow / ec choice.
+// Returns hipSuccess or the launch error.  Arguments are already validated.
+hipError_t launch_gemm(const GemmArgs& a, int tile, int flow, bool ec, hipStream_t stream);
+
+// True if (tile, flow) is a compiled combination.
+bool gemm_variant_exists(int tile, int flow);
+
+struct HouseholderArgs {
+    int ncols;
+    const float* u;
+    int64_t su;
+    const float* B;
+    int64_t ldb, sb;
+    float* C;
+    int64_t ldc, sc;
+    int batch;
+};
+
+hipError_t launch_householder64(const HouseholderArgs& a, hipStream_t stream);
+
+hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+                        hipStream_t stream);
+
+hipError_t launch_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
+                            hipStream_t stream);
+
+}  // namespace sgemm_emu

@@ -1,0 +1,62 @@
+// Small device utilities behind the C ABI: the elementwise split (so the
+// split can be checked bit for bit against its definition) and a one-MFMA
+// probe that takes operands lane by lane (the register-level counterpart of
+// the paper's mapping probe, Sec. 2.3.2).
+#include "internal.h"
+#include "mfmae/frag.hpp"
+#include "mfmae/tcec.hpp"
+#include "sgemm_emu.h"
+
+namespace sgemm_emu {
+
+__global__ __launch_bounds__(256) void split_kernel(int64_t count, const float* __restrict__ x,
+                                                    uint16_t* __restrict__ hi,
+                                                    uint16_t* __restrict__ lo) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) {
+        _Float16 h, l;
+        mfmae::tcec::split(x[i], h, l);
+        hi[i] = __builtin_bit_cast(uint16_t, h);
+        lo[i] = __builtin_bit_cast(uint16_t, l);
+    }
+}
+
+hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+                        hipStream_t stream) {
+    if (count == 0) return hipSuccess;
+    int64_t blocks = (count + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(split_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, count, x, hi, lo);
+    return hipGetLastError();
+}
+
+template <class S>
+__global__ __launch_bounds__(64) void mma_probe_kernel(const uint16_t* __restrict__ a,
+                                                       const uint16_t* __restrict__ b,
+                                                       float* __restrict__ d) {
+    const int l = threadIdx.x;
+    mfmae::half8_t va, vb;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        va[e] = __builtin_bit_cast(_Float16, a[l * 8 + e]);
+        vb[e] = __builtin_bit_cast(_Float16, b[l * 8 + e]);
+    }
+    constexpr int n = mfmae::layout<S, mfmae::Use::Acc>::num_elements;
+    typename mfmae::tcec::acc_vec<S>::type acc;
+#pragma unroll
+    for (int e = 0; e < n; ++e) acc[e] = 0.0f;
+    acc = mfmae::mma(S{}, va, vb, acc);
+#pragma unroll
+    for (int e = 0; e < n; ++e) d[l * n + e] = acc[e];
+}
+
+hipError_t launch_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
+                            hipStream_t stream) {
+    if (shape == MFMAE_SHAPE_16x16x32)
+        hipLaunchKernelGGL(mma_probe_kernel<mfmae::Shape16>, dim3(1), dim3(64), 0, stream, a, b, d);
+    else
+        hipLaunchKernelGGL(mma_probe_kernel<mfmae::Shape32>, dim3(1), dim3(64), 0, stream, a, b, d);
+    return hipGetLastError();
+}
+
+}  // namespace sgemm_emu

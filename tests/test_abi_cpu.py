@@ -1,0 +1,206 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+* the library loads and exports every function include/sgemm_emu.h declares;
+* every invalid argument is rejected with its documented code before any HIP
+  call (the fake device pointers below are never dereferenced);
+* empty problems are successful no-ops;
+* the fragment maps are bijections and map/foreach are mutually inverse.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2308_15152_amd as pkg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sgemm_emu.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declarations_match_binding():
+    assert _declared_functions() == sorted(pkg.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pkg.load()
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", pkg.lib_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for name in _declared_functions():
+        assert name in exported, name
+
+
+# fake, well separated device addresses: validation must reject or no-op
+# before anything would touch them
+PA, PB, PC = 0x10000000, 0x20000000, 0x30000000
+S = pkg.Stride
+
+
+def gemm(m, n, k, A=PA, lda=None, B=PB, ldb=None, C=PC, ldc=None, batch=1, st=(0, 0, 0),
+         policy=None):
+    lib = pkg.load()
+    lda = k if lda is None else lda
+    ldb = n if ldb is None else ldb
+    ldc = n if ldc is None else ldc
+    args = (m, n, k, ctypes.c_void_p(A), max(lda, 0), ctypes.c_void_p(B), max(ldb, 0),
+            ctypes.c_void_p(C), max(ldc, 0), batch, S(*st))
+    if policy is None:
+        return lib.sgemm_emu_batched(*args, ctypes.c_void_p(0))
+    return lib.sgemm_emu_batched_ex(*args, ctypes.byref(policy), ctypes.c_void_p(0))
+
+
+@pytest.mark.parametrize("dims", [(-1, 4, 4), (4, -1, 4), (4, 4, -1)])
+def test_negative_dims(dims):
+    assert gemm(*dims) == -1
+
+
+def test_negative_batch():
+    assert gemm(4, 4, 4, batch=-2) == -1
+
+
+def test_leading_dimensions():
+    assert gemm(4, 8, 16, lda=15) == -2
+    assert gemm(4, 8, 16, ldb=7) == -2
+    assert gemm(4, 8, 16, ldc=7) == -2
+    assert gemm(4, 8, 0, lda=0) == -2  # lda >= max(1, k)
+
+
+def test_null_pointers():
+    assert gemm(4, 4, 4, C=0) == -3
+    assert gemm(4, 4, 4, A=0) == -3
+    assert gemm(4, 4, 4, B=0) == -3
+
+
+def test_strides():
+    assert gemm(4, 4, 4, batch=2, st=(-16, 16, 16)) == -4
+    assert gemm(4, 4, 4, batch=2, st=(16, 16, 15)) == -4  # C items would overlap
+
+
+def test_aliasing():
+    assert gemm(4, 4, 4, C=PA) == -5
+    assert gemm(4, 4, 4, C=PB + 8) == -5
+    # the last C item reaches into B
+    assert gemm(4, 4, 4, C=PB - 3 * 16 * 4, batch=4, st=(16, 16, 16)) == -5
+
+
+def test_policy_values():
+    assert gemm(4, 4, 4, policy=pkg.Policy(flow=7)) == -8
+    assert gemm(4, 4, 4, policy=pkg.Policy(ec=2)) == -8
+    assert gemm(4, 4, 4, policy=pkg.Policy(tile=9)) == -8
+    # LDS of the staged flow does not fit the largest tile
+    assert gemm(4, 4, 4, policy=pkg.Policy(flow=pkg.FLOW_STAGED, tile=pkg.TILE_256x128)) == -8
+
+
+def test_empty_problems_are_noops():
+    assert gemm(0, 4, 4) == 0
+    assert gemm(4, 0, 4, ldb=1, ldc=1) == 0
+    assert gemm(4, 4, 4, batch=0) == 0
+    assert gemm(0, 4, 4, A=0, B=0, C=0) == 0
+
+
+def test_householder_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+
+    def hh(n=64, u=PA, su=64, B=PB, ldb=64, sb=4096, ncols=64, C=PC, ldc=64, sc=4096, batch=2):
+        return lib.householder_emu_batched(n, P(u), su, P(B), ldb, sb, ncols, P(C), ldc, sc,
+                                           batch, P(0))
+
+    assert hh(n=-1) == -1
+    assert hh(ncols=-1) == -1
+    assert hh(ldb=63) == -2
+    assert hh(n=32) == -6
+    assert hh(u=0) == -3
+    assert hh(sb=-1) == -4
+    assert hh(sc=100) == -4
+    assert hh(C=PB) == -5
+    assert hh(C=PA + 4) == -5
+    assert hh(batch=0) == 0
+    assert hh(ncols=0) == 0
+
+
+def test_split_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    assert lib.sgemm_emu_split(-1, P(PA), P(PB), P(PC), P(0)) == -1
+    assert lib.sgemm_emu_split(0, P(0), P(0), P(0), P(0)) == 0
+    assert lib.sgemm_emu_split(16, P(0), P(PB), P(PC), P(0)) == -3
+    assert lib.sgemm_emu_split(16, P(PA), P(PA + 8), P(PC), P(0)) == -5
+
+
+def test_strerror_covers_codes():
+    for code in range(-8, 1):
+        assert "unknown" not in pkg.sgemm_emu_strerror(code)
+    assert "unknown" in pkg.sgemm_emu_strerror(-99)
+
+
+# --------------------------------------------------------------------------
+# fragment maps
+# --------------------------------------------------------------------------
+DIMS = {  # (shape, use) -> (rows, cols, elements per lane)
+    (pkg.SHAPE_16x16x32, pkg.USE_A): (16, 32, 8),
+    (pkg.SHAPE_16x16x32, pkg.USE_B): (32, 16, 8),
+    (pkg.SHAPE_16x16x32, pkg.USE_ACC): (16, 16, 4),
+    (pkg.SHAPE_32x32x16, pkg.USE_A): (32, 16, 8),
+    (pkg.SHAPE_32x32x16, pkg.USE_B): (16, 32, 8),
+    (pkg.SHAPE_32x32x16, pkg.USE_ACC): (32, 32, 16),
+}
+
+
+@pytest.mark.parametrize("shape,use", list(DIMS))
+def test_map_is_bijection_and_inverse_of_foreach(shape, use):
+    rows, cols, ne = DIMS[(shape, use)]
+    assert pkg.mfmae_num_elements(shape, use) == ne
+    seen = {}
+    for i in range(rows):
+        for j in range(cols):
+            lane, elem = pkg.mfmae_map(shape, use, i, j)
+            assert 0 <= lane < 64 and 0 <= elem < ne
+            assert (lane, elem) not in seen
+            seen[(lane, elem)] = (i, j)
+    assert len(seen) == 64 * ne
+    for lane in range(64):
+        for elem, (i, j) in enumerate(pkg.mfmae_foreach(shape, use, lane)):
+            assert seen[(lane, elem)] == (i, j)
+
+
+def test_map_structure():
+    """Row of A and column of B/C are a function of the lane alone (one
+    element per lane per row), and the 8 elements of an A/B lane are 8
+    consecutive k; C's 32x32 layout interleaves 4-row groups of the two
+    half-waves."""
+    for shape, m in ((pkg.SHAPE_16x16x32, 16), (pkg.SHAPE_32x32x16, 32)):
+        for lane in range(64):
+            a = pkg.mfmae_foreach(shape, pkg.USE_A, lane)
+            assert len({i for i, _ in a}) == 1 and a[0][0] == lane % m
+            ks = [j for _, j in a]
+            assert ks == list(range(ks[0], ks[0] + 8)) and ks[0] % 8 == 0
+            b = pkg.mfmae_foreach(shape, pkg.USE_B, lane)
+            assert len({j for _, j in b}) == 1 and b[0][1] == lane % m
+            assert [i for i, _ in b] == ks  # the same k set as A on this lane
+    acc = pkg.mfmae_foreach(pkg.SHAPE_32x32x16, pkg.USE_ACC, 33)
+    assert [i for i, _ in acc] == [4, 5, 6, 7, 12, 13, 14, 15, 20, 21, 22, 23, 28, 29, 30, 31]
+    assert {j for _, j in acc} == {1}
+
+
+def test_map_rejects_out_of_range():
+    lib = pkg.load()
+    lane, elem = ctypes.c_int(), ctypes.c_int()
+    assert lib.mfmae_map(0, 0, 16, 0, ctypes.byref(lane), ctypes.byref(elem)) == -1
+    assert lib.mfmae_map(1, 0, 0, 16, ctypes.byref(lane), ctypes.byref(elem)) == -1
+    assert lib.mfmae_map(2, 0, 0, 0, ctypes.byref(lane), ctypes.byref(elem)) == -6
+    assert lib.mfmae_map(0, 3, 0, 0, ctypes.byref(lane), ctypes.byref(elem)) == -6
+    assert lib.mfmae_num_elements(0, 5) == -6
+    ii = (ctypes.c_int * 16)()
+    assert lib.mfmae_foreach(0, 0, 64, ii, ii) == -1

@@ -1,0 +1,209 @@
+"""Parity of the batched emulated SGEMM (Sec. 4.4) against the oracle, through
+the C ABI on the GPU.
+
+* every policy (split flow, direct flow, staged flow; error correction on and
+  off; every tile) on shapes that span several tiles and ragged tails;
+* edge cases: k = 0, empty problems, a single element, broadcast operands
+  (zero batch stride), padded leading dimensions, unaligned pointers (the
+  scalar-load path);
+* exactness on integer inputs in binary16 range;
+* the error-correction-off control must be visibly worse (the correction
+  terms are live);
+* determinism (no atomics, no split-k);
+* the full-size workloads in the launch configuration the benchmark times,
+  checked on sampled items / elements.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2308_15152_amd as pkg
+import synth
+from gpu_util import device, gate, to_np
+
+pytestmark = pytest.mark.gpu
+
+POLICIES = [
+    pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_64x64),
+    pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_128x128),
+    pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128),
+    pkg.Policy(pkg.FLOW_DIRECT, 1, pkg.TILE_64x64),
+    pkg.Policy(pkg.FLOW_DIRECT, 1, pkg.TILE_128x128),
+    pkg.Policy(pkg.FLOW_DIRECT, 1, pkg.TILE_256x128),
+    pkg.Policy(pkg.FLOW_STAGED, 1, pkg.TILE_64x64),
+    pkg.Policy(pkg.FLOW_STAGED, 1, pkg.TILE_128x128),
+]
+
+
+def _pid(p):
+    return f"flow{p.flow}-ec{p.ec}-tile{p.tile}"
+
+
+def _run(A, B, policy=None, C=None):
+    dev = device()
+    Ad = A.to(dev) if A.device.type == "cpu" else A
+    Bd = B.to(dev) if B.device.type == "cpu" else B
+    return to_np(pkg.sgemm_emu_batched(Ad, Bd, C, policy=policy))
+
+
+SHAPES = [  # batch, m, n, k
+    (2, 64, 64, 64),
+    (3, 130, 77, 65),
+    (1, 257, 129, 96),
+    (2, 17, 33, 300),
+    (1, 1, 1, 1),
+    (2, 3, 5, 7),
+    (1, 300, 260, 33),
+]
+
+
+@pytest.mark.parametrize("policy", POLICIES, ids=_pid)
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_policies_ragged_shapes(policy, shape):
+    batch, m, n, k = shape
+    print(f"case policy={_pid(policy)} shape={shape}", flush=True)
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=11 + m + n + k)
+    C = _run(A, B, policy)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(C, ref, k, f"{_pid(policy)} {shape}")
+
+
+@pytest.mark.parametrize("policy", POLICIES, ids=_pid)
+def test_integer_inputs_exact(policy):
+    g = synth.rng(7)
+    A = synth.integer_matrix((2, 96, 160), g, -8, 8)
+    B = synth.integer_matrix((2, 160, 72), g, -8, 8)
+    C = _run(A, B, policy)
+    ref = np.einsum("bik,bkj->bij", A.numpy().astype(np.int64), B.numpy().astype(np.int64))
+    assert np.array_equal(C, ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("flow", [pkg.FLOW_SPLIT, pkg.FLOW_DIRECT, pkg.FLOW_STAGED])
+def test_error_correction_is_live(flow):
+    """Without the two correction products the error is at the fp16 level
+    (about 2^-11 relative); with them it is at the FP32 level."""
+    A, B = synth.gemm_inputs(2, 128, 128, 128, seed=3)
+    ref = oracle.gemm(A.numpy(), B.numpy(), want=("c64", "n64", "c32"))
+    on = _run(A, B, pkg.Policy(flow, 1, pkg.TILE_128x128))
+    off = _run(A, B, pkg.Policy(flow, 0, pkg.TILE_128x128))
+    e_on = oracle.max_rel_err(on, ref["c64"], ref["n64"])
+    e_off = oracle.max_rel_err(off, ref["c64"], ref["n64"])
+    print(f"flow {flow}: ec on {e_on:.3e}, ec off {e_off:.3e}")
+    assert e_off > 2.0 ** -16
+    assert e_on < 2.0 ** -20
+    # ec off computes exactly the product of the hi parts
+    hiA = A.numpy().astype(np.float16).astype(np.float64)
+    hiB = B.numpy().astype(np.float16).astype(np.float64)
+    hh = np.einsum("bik,bkj->bij", hiA, hiB)
+    assert np.all(np.abs(off - hh) <= 130 * 2.0 ** -23 * ref["n64"])
+
+
+def test_k_zero_stores_zeros():
+    dev = device()
+    A = torch.zeros((2, 8, 0), device=dev)
+    B = torch.zeros((2, 0, 5), device=dev)
+    C = torch.full((2, 8, 5), 7.0, device=dev)
+    pkg.sgemm_emu_batched(A, B, C)
+    assert np.all(to_np(C) == 0)
+
+
+def test_empty_batch_and_rows_leave_output_untouched():
+    dev = device()
+    C = torch.full((1, 4, 4), 3.0, device=dev)
+    pkg.sgemm_emu_batched(torch.zeros((1, 0, 4), device=dev), torch.zeros((1, 4, 4), device=dev),
+                          torch.zeros((1, 0, 4), device=dev))
+    pkg.sgemm_emu_batched(torch.ones((0, 4, 4), device=dev), torch.ones((0, 4, 4), device=dev),
+                          torch.zeros((0, 4, 4), device=dev))
+    assert np.all(to_np(C) == 3.0)
+
+
+def test_broadcast_operand():
+    """A 2-D B is shared by every item (batch stride 0)."""
+    A, B = synth.gemm_inputs(4, 70, 90, 50, seed=21)
+    B0 = B[0]
+    C = _run(A, B0)
+    ref = oracle.gemm(A.numpy(), np.broadcast_to(B0.numpy(), (4, 50, 90)))
+    gate(C, ref, 50, "broadcast B")
+
+
+def test_padded_leading_dimensions_and_strides():
+    """Operands that are views into larger buffers: lda > k, ldb > n,
+    ldc > n and batch strides larger than the matrices."""
+    dev = device()
+    A_big, B_big = synth.gemm_inputs(3, 100, 140, 120, seed=23)
+    A = A_big[:, :90, :70].to(dev)
+    B = B_big[:, :70, :110].to(dev)
+    C_big = torch.full((3, 96, 128), -5.0, device=dev)
+    C = C_big[:, :90, :110]
+    pkg.sgemm_emu_batched(A, B, C)
+    out = to_np(C_big)
+    ref = oracle.gemm(A.cpu().numpy(), B.cpu().numpy())
+    gate(out[:, :90, :110], ref, 70, "padded")
+    assert np.all(out[:, 90:, :] == -5.0) and np.all(out[:, :, 110:] == -5.0)
+
+
+def test_unaligned_pointers_take_scalar_path():
+    dev = device()
+    A, B = synth.gemm_inputs(2, 65, 66, 67, seed=25)
+    flatA = torch.zeros(A.numel() + 1, device=dev)
+    flatB = torch.zeros(B.numel() + 3, device=dev)
+    flatA[1:] = A.reshape(-1).to(dev)
+    flatB[3:] = B.reshape(-1).to(dev)
+    Ad = flatA[1:].view(2, 65, 67)
+    Bd = flatB[3:].view(2, 67, 66)
+    C = to_np(pkg.sgemm_emu_batched(Ad, Bd))
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(C, ref, 67, "unaligned")
+
+
+def test_deterministic():
+    A, B = synth.gemm_inputs(8, 128, 128, 128, seed=27)
+    c1 = _run(A, B)
+    c2 = _run(A, B)
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, in the configuration the benchmark times (automatic
+# policy), compared on sampled items / elements.
+# ---------------------------------------------------------------------------
+
+def _full_gemm_sampled(name, items):
+    w = synth.WORKLOADS[name]
+    print(f"case workload={name} batch={w.batch} m={w.m} n={w.n} k={w.k}", flush=True)
+    A, B = synth.workload_inputs(w)
+    C = _run(A, B)
+    assert C.shape == (w.batch, w.m, w.n)
+    ref = oracle.gemm(A[items].numpy(), B[items].numpy())
+    return gate(C[items], ref, w.k, name)
+
+
+def test_workload_gemm_64_full():
+    w = synth.WORKLOADS["gemm_64"]
+    _full_gemm_sampled("gemm_64", list(range(w.batch)))
+
+
+def test_workload_gemm_128_sampled():
+    e = _full_gemm_sampled("gemm_128", [0, 1, 777, 2048, 4000, 4095])
+    print(f"gemm_128: err {e[0]:.3e} fp32 {e[1]:.3e}")
+
+
+def test_workload_gemm_256e_sampled():
+    e = _full_gemm_sampled("gemm_256e", [0, 511, 1023])
+    print(f"gemm_256e: err {e[0]:.3e} fp32 {e[1]:.3e}")
+
+
+def test_workload_gemm_8192_sampled():
+    w = synth.WORKLOADS["gemm_8192"]
+    print("case workload=gemm_8192", flush=True)
+    A, B = synth.workload_inputs(w)
+    C = _run(A, B)[0]
+    g = np.random.default_rng(8192)
+    rows = np.concatenate([g.integers(0, w.m, 500), [0, w.m - 1, 0, w.m - 1]])
+    cols = np.concatenate([g.integers(0, w.n, 500), [0, 0, w.n - 1, w.n - 1]])
+    An = A[0].numpy()
+    Bn = B[0].numpy()
+    ref = oracle.dots(An[rows], np.ascontiguousarray(Bn[:, cols].T))
+    e = gate(C[rows, cols], ref, w.k, "gemm_8192")
+    print(f"gemm_8192: err {e[0]:.3e} fp32 {e[1]:.3e}")
