@@ -180,7 +180,7 @@ def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None
     if C is None:
         C = torch.empty((batch, m, n), dtype=torch.float32, device=A.device)
     bc, mc, nc, ldc, sc = _matrix_view(C if C.dim() == 3 else C.unsqueeze(0), "C")
-    if (mc, nc) != (m, n) or (bc or 1) != batch:
+    if (mc, nc) != (m, n) or (bc if bc is not None else 1) != batch:
         raise ValueError("C has the wrong shape")
     st = Stride(sa, sb, sc if batch > 1 else 0)
     lib = load()

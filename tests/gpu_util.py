@@ -11,7 +11,18 @@ not specified):
   split taken exactly, summed in FP64): every FP32 addition on the device
   path moves the result by at most one ulp of a partial sum bounded by N
   (for round-to-nearest half an ulp; one ulp also covers truncation), so
-      |C - CM|_ij <= (k + 2) * 2^-23 * N_ij.
+      |C - CM|_ij <= (k + 2) * 2^-23 * N_ij;
+* element by element against the FP64 product: the split represents each
+  operand to within 2^-22 of its magnitude and the dropped lo.lo term is at
+  most 2^-22 |a||b|, so each product is off by at most about 3 * 2^-22 |a||b|
+  before accumulation, and
+      |C - C64|_ij <= (k + 8) * 2^-23 * N_ij.
+
+The two max-error gates compare statistics of rounding errors.  With a
+handful of terms the plain FP32 chain can be exact by chance (k = 1 is one
+correctly rounded product), so the ratio says nothing there; the gates are
+applied to every workload and to every shape with k >= 32 and at least 256
+outputs, and the element-wise bounds to every shape.
 """
 from __future__ import annotations
 
@@ -28,15 +39,23 @@ def device():
     return torch.device("cuda:0")
 
 
-def gate(C, ref, k, label=""):
-    """Assert the accuracy gate and the element-wise model bound; return the
-    errors for reporting."""
+def gate_applies(k, outputs) -> bool:
+    return k >= 32 and outputs >= 256
+
+
+def gate(C, ref, k, label="", max_gate=True):
+    """Assert the element-wise bounds and (if ``max_gate``) the accuracy gate;
+    return the errors for reporting."""
     C = np.asarray(C, dtype=np.float32)
     assert np.isfinite(C).all(), f"{label}: non-finite output"
     e_emu = oracle.max_rel_err(C, ref["c64"], ref["n64"])
     e_32 = oracle.max_rel_err(ref["c32"], ref["c64"], ref["n64"])
-    assert e_emu <= 2 * e_32, f"{label}: err {e_emu:.3e} > 2 x fp32 err {e_32:.3e}"
-    assert e_emu <= max(k, 1) * 2.0 ** -23, f"{label}: err {e_emu:.3e} > k 2^-23"
+    if max_gate:
+        assert e_emu <= 2 * e_32, f"{label}: err {e_emu:.3e} > 2 x fp32 err {e_32:.3e}"
+        assert e_emu <= max(k, 1) * 2.0 ** -23, f"{label}: err {e_emu:.3e} > k 2^-23"
+    dev64 = np.abs(C.astype(np.float64) - ref["c64"])
+    bad = dev64 > (k + 8) * 2.0 ** -23 * ref["n64"]
+    assert not bad.any(), f"{label}: {int(bad.sum())} elements beyond (k+8) 2^-23 N"
     if "cm" in ref:
         dev = np.abs(C.astype(np.float64) - ref["cm"])
         bound = (k + 2) * 2.0 ** -23 * ref["n64"]
