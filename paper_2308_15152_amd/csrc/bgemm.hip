@@ -37,6 +37,7 @@
 #include <type_traits>
 
 #include "internal.h"
+#include "tiling.hpp"
 #include "mfmae/frag.hpp"
 #include "mfmae/tcec.hpp"
 #include "sgemm_emu.h"
@@ -52,7 +53,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 enum { FLOW_SPLIT = SGEMM_EMU_FLOW_SPLIT, FLOW_DIRECT = SGEMM_EMU_FLOW_DIRECT,
        FLOW_STAGED = SGEMM_EMU_FLOW_STAGED };
 
-constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Split four FP32 values into packed hi and lo halves (element e of the
 // input goes to half e of the output pairs).
@@ -98,48 +98,6 @@ struct Cfg {
     // per SIMD cap a wave at 256 registers (VGPR + AGPR).
     static constexpr int MIN_WAVES = 2;
 };
-
-struct KParams {
-    int m, n, k;
-    const float* A;
-    int64_t lda, sa;
-    const float* B;
-    int64_t ldb, sb;
-    float* C;
-    int64_t ldc, sc;
-    int tiles_m, tiles_n;
-    int item0;        // first batch item of this launch
-    int vec_a, vec_b;
-    int xcd_remap;    // 1 if gridDim.x is a multiple of 8
-};
-
-// ---------------------------------------------------------------------------
-// Block -> (item, tile) mapping.
-//
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
-// L2).  Renumbering so that the 1/8 of the grid an XCD receives is a
-// contiguous range of tiles keeps tiles that share A rows and B columns in
-// the same L2; within an item, tiles are visited in groups of GROUP_M tile
-// rows so that consecutive tiles reuse the same B columns.
-// ---------------------------------------------------------------------------
-__device__ inline void block_coords(const KParams& p, int& item, int& tm, int& tn) {
-    int bid = blockIdx.x;
-    if (p.xcd_remap) {
-        const int per = gridDim.x >> 3;
-        bid = (bid & 7) * per + (bid >> 3);
-    }
-    const int tiles = p.tiles_m * p.tiles_n;
-    item = bid / tiles;
-    int t = bid - item * tiles;
-    constexpr int GROUP_M = 8;
-    const int group_size = GROUP_M * p.tiles_n;
-    const int g = t / group_size;
-    const int first_m = g * GROUP_M;
-    const int gm = min(p.tiles_m - first_m, GROUP_M);
-    const int r = t - g * group_size;
-    tm = first_m + r % gm;
-    tn = r / gm;
-}
 
 // ---------------------------------------------------------------------------
 // Global -> register staging of one k chunk.
@@ -331,29 +289,67 @@ __device__ inline void stage_wave_planes(const float* as, const float* bs, _Floa
 }
 
 // ---------------------------------------------------------------------------
-// The kernel.
+// One k chunk of MFMA work from the LDS stage `cur`.
 // ---------------------------------------------------------------------------
 template <class CF>
-__global__ __launch_bounds__(CF::NT, CF::MIN_WAVES) void bgemm_emu_kernel(KParams p) {
-    static_assert(CF::FITS, "LDS budget of one CU");
-    __shared__ __attribute__((aligned(16))) unsigned char smem[CF::LDS_BYTES];
+__device__ inline void compute_chunk(f32x16_t (&acc)[CF::TM][CF::TN], f32x16_t (&cor)[CF::TM][CF::TN],
+                                     unsigned char* smem, const unsigned char* cur, int wave,
+                                     int wrow, int wcol) {
+    if constexpr (CF::FLOW == FLOW_STAGED) {
+        _Float16* scratch =
+            reinterpret_cast<_Float16*>(smem + 2 * CF::STAGE + wave * CF::WAVE_SCRATCH);
+        const float* as = reinterpret_cast<const float*>(cur);
+        stage_wave_planes<CF>(as, as + CF::BM * CF::PF, scratch, wrow, wcol);
+        __builtin_amdgcn_wave_barrier();
+    }
+#pragma unroll
+    for (int s = 0; s < CF::KSTEPS; ++s) {
+        Frags<CF> fr;
+        if constexpr (CF::FLOW == FLOW_SPLIT) {
+            const _Float16* a_hi = reinterpret_cast<const _Float16*>(cur);
+            const _Float16* a_lo = a_hi + CF::BM * CF::PH;
+            const _Float16* b_hi = a_lo + CF::BM * CF::PH;
+            const _Float16* b_lo = b_hi + CF::BN * CF::PH;
+            read_planes<CF>(a_hi, a_lo, wrow, s, fr.ahi, fr.alo);
+            read_planes<CF>(b_hi, b_lo, wcol, s, fr.bhi, fr.blo);
+        } else if constexpr (CF::FLOW == FLOW_DIRECT) {
+            const float* as = reinterpret_cast<const float*>(cur);
+            read_f32_split<CF>(as, wrow, s, fr.ahi, fr.alo);
+            read_f32_split<CF>(as + CF::BM * CF::PF, wcol, s, fr.bhi, fr.blo);
+        } else {
+            const _Float16* a_hi =
+                reinterpret_cast<const _Float16*>(smem + 2 * CF::STAGE + wave * CF::WAVE_SCRATCH);
+            const _Float16* a_lo = a_hi + CF::WM * CF::PH;
+            const _Float16* b_hi = a_lo + CF::WM * CF::PH;
+            const _Float16* b_lo = b_hi + CF::WN * CF::PH;
+            read_planes<CF>(a_hi, a_lo, 0, s, fr.ahi, fr.alo);
+            read_planes<CF>(b_hi, b_lo, 0, s, fr.bhi, fr.blo);
+        }
+#pragma unroll
+        for (int i = 0; i < CF::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < CF::TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.ahi[i], fr.bhi[j], acc[i][j],
+                                                                   0, 0, 0);
+        if constexpr (CF::EC) {
+#pragma unroll
+            for (int i = 0; i < CF::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < CF::TN; ++j)
+                    cor[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.alo[i], fr.bhi[j],
+                                                                       cor[i][j], 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < CF::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < CF::TN; ++j)
+                    cor[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.ahi[i], fr.blo[j],
+                                                                       cor[i][j], 0, 0, 0);
+        }
+    }
+}
 
-    int item, tile_m, tile_n;
-    block_coords(p, item, tile_m, tile_n);
-    item += p.item0;
-    const int m0 = tile_m * CF::BM;
-    const int n0 = tile_n * CF::BN;
-
-    const float* __restrict__ Ab = p.A + (int64_t)item * p.sa;
-    const float* __restrict__ Bb = p.B + (int64_t)item * p.sb;
-    float* __restrict__ Cb = p.C + (int64_t)item * p.sc;
-
-    const int wave = threadIdx.x >> 6;
-    const int l = threadIdx.x & 63;
-    const int wrow = (wave / CF::WAVES_N) * CF::WM;  // within the tile
-    const int wcol = (wave % CF::WAVES_N) * CF::WN;
-
-    f32x16_t acc[CF::TM][CF::TN], cor[CF::TM][CF::TN];
+template <class CF>
+__device__ inline void zero_acc(f32x16_t (&acc)[CF::TM][CF::TN], f32x16_t (&cor)[CF::TM][CF::TN]) {
 #pragma unroll
     for (int i = 0; i < CF::TM; ++i)
 #pragma unroll
@@ -363,95 +359,93 @@ __global__ __launch_bounds__(CF::NT, CF::MIN_WAVES) void bgemm_emu_kernel(KParam
                 acc[i][j][e] = 0.0f;
                 cor[i][j][e] = 0.0f;
             }
+}
 
-    const int nchunks = cdiv(p.k, CF::BK);
-    Stage<CF> st;
-    if (nchunks > 0) {
-        load_chunk<CF>(st, p, Ab, Bb, m0, n0, 0);
-        store_chunk<CF>(st, smem);
-    }
-    __syncthreads();
-
-    for (int c = 0; c < nchunks; ++c) {
-        unsigned char* cur = smem + (c & 1) * CF::STAGE;
-        unsigned char* nxt = smem + ((c + 1) & 1) * CF::STAGE;
-        const bool more = c + 1 < nchunks;
-        if (more) load_chunk<CF>(st, p, Ab, Bb, m0, n0, (c + 1) * CF::BK);
-
-        if constexpr (CF::FLOW == FLOW_STAGED) {
-            _Float16* scratch = reinterpret_cast<_Float16*>(smem + 2 * CF::STAGE +
-                                                            wave * CF::WAVE_SCRATCH);
-            const float* as = reinterpret_cast<const float*>(cur);
-            stage_wave_planes<CF>(as, as + CF::BM * CF::PF, scratch, wrow, wcol);
-            __builtin_amdgcn_wave_barrier();
-        }
-
-#pragma unroll
-        for (int s = 0; s < CF::KSTEPS; ++s) {
-            Frags<CF> fr;
-            if constexpr (CF::FLOW == FLOW_SPLIT) {
-                const _Float16* a_hi = reinterpret_cast<const _Float16*>(cur);
-                const _Float16* a_lo = a_hi + CF::BM * CF::PH;
-                const _Float16* b_hi = a_lo + CF::BM * CF::PH;
-                const _Float16* b_lo = b_hi + CF::BN * CF::PH;
-                read_planes<CF>(a_hi, a_lo, wrow, s, fr.ahi, fr.alo);
-                read_planes<CF>(b_hi, b_lo, wcol, s, fr.bhi, fr.blo);
-            } else if constexpr (CF::FLOW == FLOW_DIRECT) {
-                const float* as = reinterpret_cast<const float*>(cur);
-                read_f32_split<CF>(as, wrow, s, fr.ahi, fr.alo);
-                read_f32_split<CF>(as + CF::BM * CF::PF, wcol, s, fr.bhi, fr.blo);
-            } else {
-                const _Float16* a_hi = reinterpret_cast<const _Float16*>(smem + 2 * CF::STAGE +
-                                                                         wave * CF::WAVE_SCRATCH);
-                const _Float16* a_lo = a_hi + CF::WM * CF::PH;
-                const _Float16* b_hi = a_lo + CF::WM * CF::PH;
-                const _Float16* b_lo = b_hi + CF::WN * CF::PH;
-                read_planes<CF>(a_hi, a_lo, 0, s, fr.ahi, fr.alo);
-                read_planes<CF>(b_hi, b_lo, 0, s, fr.bhi, fr.blo);
-            }
-#pragma unroll
-            for (int i = 0; i < CF::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < CF::TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.ahi[i], fr.bhi[j],
-                                                                       acc[i][j], 0, 0, 0);
-            if constexpr (CF::EC) {
-#pragma unroll
-                for (int i = 0; i < CF::TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < CF::TN; ++j)
-                        cor[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.alo[i], fr.bhi[j],
-                                                                           cor[i][j], 0, 0, 0);
-#pragma unroll
-                for (int i = 0; i < CF::TM; ++i)
-#pragma unroll
-                    for (int j = 0; j < CF::TN; ++j)
-                        cor[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fr.ahi[i], fr.blo[j],
-                                                                           cor[i][j], 0, 0, 0);
-            }
-        }
-
-        if (more) store_chunk<CF>(st, nxt);
-        __syncthreads();
-    }
-
-    // Epilogue: C = main + corr * 2^-11, accumulator layout of the 32x32 MFMA:
-    // element e of lane l is row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32.
-    const bool full = (m0 + CF::BM <= p.m) && (n0 + CF::BN <= p.n);
+// Epilogue: C = main + corr * 2^-11, accumulator layout of the 32x32 MFMA:
+// element e of lane l is row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32.
+template <class CF>
+__device__ inline void store_tile(const f32x16_t (&acc)[CF::TM][CF::TN],
+                                  const f32x16_t (&cor)[CF::TM][CF::TN], const KParams& p,
+                                  const TaskPos& q, int wrow, int wcol) {
+    const int l = threadIdx.x & 63;
+    const bool full = (q.m0 + CF::BM <= p.m) && (q.n0 + CF::BN <= p.n);
 #pragma unroll
     for (int i = 0; i < CF::TM; ++i)
 #pragma unroll
         for (int j = 0; j < CF::TN; ++j) {
-            const int col = n0 + wcol + 32 * j + (l & 31);
+            const int col = q.n0 + wcol + 32 * j + (l & 31);
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int row = m0 + wrow + 32 * i + 8 * (e >> 2) + 4 * (l >> 5) + (e & 3);
+                const int row = q.m0 + wrow + 32 * i + 8 * (e >> 2) + 4 * (l >> 5) + (e & 3);
                 const float v = CF::EC ? __builtin_fmaf(cor[i][j][e], mfmae::tcec::kLoScaleInv,
                                                         acc[i][j][e])
                                        : acc[i][j][e];
-                if (full || (row < p.m && col < p.n)) Cb[(int64_t)row * p.ldc + col] = v;
+                if (full || (row < p.m && col < p.n)) q.C[(int64_t)row * p.ldc + col] = v;
             }
         }
+}
+
+// ---------------------------------------------------------------------------
+// The kernel.
+// ---------------------------------------------------------------------------
+template <class CF>
+__global__ __launch_bounds__(CF::NT, CF::MIN_WAVES) void bgemm_emu_kernel(KParams p) {
+    static_assert(CF::FITS, "LDS budget of one CU");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[CF::LDS_BYTES];
+
+    const int G = gridDim.x;
+    int task = first_task(p);
+    if (task >= p.ntasks) return;  // the whole workgroup leaves together
+
+    const int wave = threadIdx.x >> 6;
+    const int wrow = (wave / CF::WAVES_N) * CF::WM;  // within the tile
+    const int wcol = (wave % CF::WAVES_N) * CF::WN;
+
+    f32x16_t acc[CF::TM][CF::TN], cor[CF::TM][CF::TN];
+    zero_acc<CF>(acc, cor);
+
+    const int nchunks = cdiv(p.k, CF::BK);
+    if (nchunks == 0) {  // empty sum: every tile is zero
+        for (; task < p.ntasks; task += G) store_tile<CF>(acc, cor, p, task_pos<CF::BM, CF::BN>(p, task), wrow, wcol);
+        return;
+    }
+
+    TaskPos cur_t = task_pos<CF::BM, CF::BN>(p, task);
+    Stage<CF> st;
+    load_chunk<CF>(st, p, cur_t.A, cur_t.B, cur_t.m0, cur_t.n0, 0);
+    store_chunk<CF>(st, smem);
+    __syncthreads();
+
+    int c = 0, buf = 0;
+    for (;;) {
+        // the chunk after this one: the next k chunk of this task, or the
+        // first chunk of this workgroup's next task
+        int ntask = task, nc = c + 1;
+        if (nc == nchunks) {
+            ntask += G;
+            nc = 0;
+        }
+        const bool more = ntask < p.ntasks;
+        TaskPos next_t = cur_t;
+        if (more) {
+            if (ntask != task) next_t = task_pos<CF::BM, CF::BN>(p, ntask);
+            load_chunk<CF>(st, p, next_t.A, next_t.B, next_t.m0, next_t.n0, nc * CF::BK);
+        }
+
+        compute_chunk<CF>(acc, cor, smem, smem + buf * CF::STAGE, wave, wrow, wcol);
+
+        if (c == nchunks - 1) {
+            store_tile<CF>(acc, cor, p, cur_t, wrow, wcol);
+            zero_acc<CF>(acc, cor);
+        }
+        if (more) store_chunk<CF>(st, smem + (buf ^ 1) * CF::STAGE);
+        __syncthreads();
+        if (!more) break;
+        task = ntask;
+        cur_t = next_t;
+        c = nc;
+        buf ^= 1;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -481,6 +475,25 @@ constexpr bool variant_fits() {
     return CfgOf<TILE, FLOW, true>::FITS;
 }
 
+// Workgroups of one instance that fit on the device at once (cached; the
+// device of the calling thread is used).
+template <class CF>
+static int resident_blocks() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cache[dev] > 0) return cache[dev];
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, bgemm_emu_kernel<CF>, CF::NT, 0) !=
+        hipSuccess)
+        return 0;
+    const int r = cus * (per_cu > 0 ? per_cu : 1);
+    cache[dev] = r;  // benign race: every thread computes the same value
+    return r;
+}
+
 template <class CF>
 static hipError_t launch_cfg(const GemmArgs& a, hipStream_t stream) {
     KParams p;
@@ -501,13 +514,21 @@ static hipError_t launch_cfg(const GemmArgs& a, hipStream_t stream) {
     p.vec_a = a.vec_a;
     p.vec_b = a.vec_b;
     const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
-    // Keep one launch below 2^31 work-items; split the batch otherwise.
-    const int64_t max_blocks = (int64_t(1) << 31) / CF::NT - 1;
-    const int64_t items_per_launch = tiles > max_blocks ? 0 : max_blocks / tiles;
-    if (items_per_launch == 0) return hipErrorInvalidConfiguration;
+    // task ids are 32-bit: split a batch whose task count would not fit
+    const int64_t max_tasks = (int64_t(1) << 31) - 1;
+    if (tiles > max_tasks) return hipErrorInvalidConfiguration;
+    const int64_t items_per_launch = max_tasks / tiles;
+    int resident = resident_blocks<CF>();
+    if (resident <= 0) {
+        hipError_t e = hipGetLastError();
+        return e != hipSuccess ? e : hipErrorInvalidDeviceFunction;
+    }
     for (int64_t i0 = 0; i0 < a.batch; i0 += items_per_launch) {
         const int64_t items = a.batch - i0 < items_per_launch ? a.batch - i0 : items_per_launch;
-        const int64_t blocks = items * tiles;
+        const int64_t ntasks = items * tiles;
+        int64_t blocks = ntasks < resident ? ntasks : resident;
+        if (blocks >= 8) blocks -= blocks % 8;
+        p.ntasks = (int)ntasks;
         p.item0 = (int)i0;
         p.xcd_remap = (blocks % 8 == 0) ? 1 : 0;
         hipLaunchKernelGGL(bgemm_emu_kernel<CF>, dim3((unsigned)blocks), dim3(CF::NT), 0, stream, p);
