@@ -25,31 +25,47 @@ namespace tcec {
 constexpr float kLoScale = 2048.0f;            // 2^11
 constexpr float kLoScaleInv = 1.0f / 2048.0f;  // 2^-11, exact
 
-// Split one value.
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Split one value.  The residual is formed as fma(hi, -2^11, x * 2^11): the
+// product x * 2^11 is exact and so is the fused result 2^11 (x - hi), which
+// is rounded once, to binary16 -- the same two roundings as the definition.
+// (gfx950 evaluates the fma with hi read straight from its binary16 register,
+// v_fma_mix, so the residual costs two instructions.)
 __device__ inline void split(float x, _Float16& hi, _Float16& lo) {
     hi = static_cast<_Float16>(x);
-    lo = static_cast<_Float16>((x - static_cast<float>(hi)) * kLoScale);
+    lo = static_cast<_Float16>(__builtin_fmaf(static_cast<float>(hi), -kLoScale, x * kLoScale));
+}
+
+// Split two values: hi is converted as a pair (one v_cvt_pk_f16_f32) and the
+// two residuals read their hi halves from that packed register.
+__device__ inline void split_pair(float x0, float x1, half2_t& hi, half2_t& lo) {
+    hi = __builtin_convertvector(f32x2_t{x0, x1}, half2_t);
+    lo[0] = static_cast<_Float16>(
+        __builtin_fmaf(static_cast<float>(hi[0]), -kLoScale, x0 * kLoScale));
+    lo[1] = static_cast<_Float16>(
+        __builtin_fmaf(static_cast<float>(hi[1]), -kLoScale, x1 * kLoScale));
 }
 
 // Split two values into packed (low half = first value) hi and lo words.
 __device__ inline void split2(float x0, float x1, uint32_t& hi2, uint32_t& lo2) {
-    _Float16 h0, h1, l0, l1;
-    split(x0, h0, l0);
-    split(x1, h1, l1);
-    hi2 = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h0)) |
-          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h1)) << 16);
-    lo2 = static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l0)) |
-          (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, l1)) << 16);
+    half2_t h, l;
+    split_pair(x0, x1, h, l);
+    hi2 = __builtin_bit_cast(uint32_t, h);
+    lo2 = __builtin_bit_cast(uint32_t, l);
 }
 
 // Split eight consecutive values into one hi and one lo operand vector.
 __device__ inline void split8(const float (&x)[8], half8_t& hi, half8_t& lo) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        _Float16 h, l;
-        split(x[e], h, l);
-        hi[e] = h;
-        lo[e] = l;
+    for (int e = 0; e < 8; e += 2) {
+        half2_t h, l;
+        split_pair(x[e], x[e + 1], h, l);
+        hi[e] = h[0];
+        hi[e + 1] = h[1];
+        lo[e] = l[0];
+        lo[e + 1] = l[1];
     }
 }
 

@@ -80,7 +80,9 @@ int sgemm_emu_batched(int m, int n, int k,
  * applied, and where the split happens.
  *
  * flow:
- *   SGEMM_EMU_FLOW_AUTO   library choice (currently SPLIT for every shape).
+ *   SGEMM_EMU_FLOW_AUTO   library choice: REG for products up to 1024 x 1024
+ *                         whose operands allow its vector loads, SPLIT
+ *                         otherwise.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
  *                         global load and the LDS store; LDS holds hi and lo
  *                         (the same 4 bytes per element as FP32) and the
@@ -94,6 +96,18 @@ int sgemm_emu_batched(int m, int n, int k,
  *                         fragments (the flow forced by a load-only fragment
  *                         API, Fig. 6 top).  Measurement only: three LDS
  *                         passes per element instead of one.
+ *   SGEMM_EMU_FLOW_REG    no LDS: every wave loads its operand elements from
+ *                         global memory straight into registers, splits them
+ *                         there and runs its MFMAs (fragments built without
+ *                         shared memory, Sec. 4.2); no barriers, so all waves
+ *                         stream independently.  For HBM-bound batches of
+ *                         small products.  Needs 16-byte aligned A rows
+ *                         (A 16-byte aligned, lda and stride.a multiples of
+ *                         4, lda < 2^23, ldb < 2^25) and, for tile 128x128,
+ *                         B vectors of 4 (B 16-byte aligned, ldb, stride.b
+ *                         and n multiples of 4) or else of 2 (8-byte
+ *                         aligned, even); tiles 64x64 and 128x128 only.
+ *                         Otherwise SGEMM_EMU_ERR_POLICY.
  * ec:   1 = error correction (3 products), 0 = hi.hi only (accuracy control).
  * tile: 0 = automatic, or one of SGEMM_EMU_TILE_*.
  */
@@ -101,11 +115,12 @@ int sgemm_emu_batched(int m, int n, int k,
 #define SGEMM_EMU_FLOW_SPLIT 1
 #define SGEMM_EMU_FLOW_DIRECT 2
 #define SGEMM_EMU_FLOW_STAGED 3
+#define SGEMM_EMU_FLOW_REG 4
 
 #define SGEMM_EMU_TILE_AUTO 0
-#define SGEMM_EMU_TILE_64x64 1   /* 4 waves of 32x32, k-chunk 32   */
-#define SGEMM_EMU_TILE_128x128 2 /* 4 waves of 64x64, k-chunk 32   */
-#define SGEMM_EMU_TILE_256x128 3 /* 8 waves of 64x64, k-chunk 32   */
+#define SGEMM_EMU_TILE_64x64 1   /* 4 waves of 32x32 (LDS flows: k-chunk 32) */
+#define SGEMM_EMU_TILE_128x128 2 /* 4 waves of 64x64 (LDS flows: k-chunk 32) */
+#define SGEMM_EMU_TILE_256x128 3 /* 8 waves of 64x64, k-chunk 32; LDS flows  */
 
 typedef struct {
     int flow;

@@ -69,14 +69,10 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
              hipStream_t stream) {
     int rc = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st);
     if (rc != SGEMM_EMU_OK) return rc;
-    if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_STAGED) return SGEMM_EMU_ERR_POLICY;
+    if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_REG) return SGEMM_EMU_ERR_POLICY;
     if (ec != 0 && ec != 1) return SGEMM_EMU_ERR_POLICY;
     if (tile < SGEMM_EMU_TILE_AUTO || tile > SGEMM_EMU_TILE_256x128) return SGEMM_EMU_ERR_POLICY;
     if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
-    if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
-    if (flow == SGEMM_EMU_FLOW_AUTO) flow = SGEMM_EMU_FLOW_SPLIT;
-    if (!sgemm_emu::gemm_variant_exists(tile, flow)) return SGEMM_EMU_ERR_POLICY;
-
     sgemm_emu::GemmArgs a;
     a.m = m;
     a.n = n;
@@ -93,7 +89,28 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
     a.batch = batch;
     a.vec_a = aligned16(A) && lda % 4 == 0 && st.a % 4 == 0;
     a.vec_b = aligned16(B) && ldb % 4 == 0 && st.b % 4 == 0;
-    hipError_t e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
+    if (flow == SGEMM_EMU_FLOW_AUTO) {
+        // Small products are bound by HBM traffic: the barrier-free
+        // register-direct flow keeps the most bytes in flight.  Large ones
+        // need the LDS-shared tiles to stay off the L2 bandwidth limit.
+        const int reg_tile = (m <= 64 && n <= 64) ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
+        if (m <= 1024 && n <= 1024 && (tile == SGEMM_EMU_TILE_AUTO || tile == reg_tile) &&
+            sgemm_emu::reg_flow_supported(a, reg_tile)) {
+            flow = SGEMM_EMU_FLOW_REG;
+            tile = reg_tile;
+        } else {
+            flow = SGEMM_EMU_FLOW_SPLIT;
+        }
+    }
+    if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
+    hipError_t e;
+    if (flow == SGEMM_EMU_FLOW_REG) {
+        if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
+        e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream);
+    } else {
+        if (!sgemm_emu::gemm_variant_exists(tile, flow)) return SGEMM_EMU_ERR_POLICY;
+        e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
+    }
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 

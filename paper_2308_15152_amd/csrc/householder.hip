@@ -33,7 +33,8 @@ struct HhParams {
     int64_t ldb, sb;
     float* C;
     int64_t ldc, sc;
-    int batch;
+    int batch;   // items of this launch
+    int64_t item0;  // first item of this launch
 };
 
 constexpr int kHhWaves = 4;  // waves (tasks) per workgroup
@@ -46,9 +47,10 @@ __global__ __launch_bounds__(64 * kHhWaves, 2) void householder64_kernel(HhParam
     // one wave per (item, group of 64 columns)
     const int64_t task = (int64_t)blockIdx.x * kHhWaves + wave;
     const int ngroups = (p.ncols + 63) / 64;
-    const int64_t item = task / ngroups;
-    const int c0 = (int)(task - item * ngroups) * 64;
-    if (item >= p.batch) return;  // whole wave; the kernel has no barrier
+    const int64_t local = task / ngroups;
+    const int c0 = (int)(task - local * ngroups) * 64;
+    if (local >= p.batch) return;  // whole wave; the kernel has no barrier
+    const int64_t item = local + p.item0;
 
     const float* __restrict__ u = p.u + item * p.su;
     const float* __restrict__ Bi = p.B + item * p.sb;
@@ -152,12 +154,23 @@ hipError_t launch_householder64(const HouseholderArgs& a, hipStream_t stream) {
     p.C = a.C;
     p.ldc = a.ldc;
     p.sc = a.sc;
-    p.batch = a.batch;
-    const int64_t tasks = (int64_t)a.batch * ((a.ncols + 63) / 64);
-    const int64_t blocks = (tasks + kHhWaves - 1) / kHhWaves;
-    hipLaunchKernelGGL(householder64_kernel, dim3((unsigned)blocks), dim3(64 * kHhWaves), 0,
-                       stream, p);
-    return hipGetLastError();
+    // one launch stays below 2^31 work-items (the dispatch packet counts
+    // work-items in 32 bits); larger batches take several launches
+    const int64_t ngroups = (a.ncols + 63) / 64;
+    const int64_t max_blocks = (int64_t(1) << 31) / (64 * kHhWaves) - 1;
+    const int64_t items_per_launch = max_blocks * kHhWaves / ngroups;
+    if (items_per_launch == 0) return hipErrorInvalidConfiguration;
+    for (int64_t i0 = 0; i0 < a.batch; i0 += items_per_launch) {
+        const int64_t items = a.batch - i0 < items_per_launch ? a.batch - i0 : items_per_launch;
+        p.batch = (int)items;
+        p.item0 = i0;
+        const int64_t blocks = (items * ngroups + kHhWaves - 1) / kHhWaves;
+        hipLaunchKernelGGL(householder64_kernel, dim3((unsigned)blocks), dim3(64 * kHhWaves), 0,
+                           stream, p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace sgemm_emu

@@ -26,6 +26,11 @@ hipError_t launch_gemm(const GemmArgs& a, int tile, int flow, bool ec, hipStream
 // True if (tile, flow) is a compiled combination.
 bool gemm_variant_exists(int tile, int flow);
 
+// Register-direct flow (no LDS): true if the operands allow its vector loads
+// for this tile choice.
+bool reg_flow_supported(const GemmArgs& a, int tile);
+hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t stream);
+
 struct HouseholderArgs {
     int ncols;
     const float* u;

@@ -50,6 +50,17 @@ __device__ inline int first_task(const KParams& p) {
     return b;
 }
 
+// Task of workgroup b in a grid of G workgroups.  Workgroups are dispatched
+// round-robin over the 8 XCDs, so b runs on XCD b % 8 as that XCD's
+// (b / 8)-th workgroup; numbering them so that every XCD receives one
+// contiguous range of task ids keeps the tiles of one item, which share A
+// rows and B columns, in one L2.  A bijection of [0, G) for any G.
+__device__ inline int xcd_task(int b, int G) {
+    const int x = b & 7, i = b >> 3;
+    const int q = G >> 3, r = G & 7;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+}
+
 struct TaskPos {
     const float* A;  // item base pointers
     const float* B;

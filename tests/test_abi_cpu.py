@@ -100,6 +100,15 @@ def test_policy_values():
     assert gemm(4, 4, 4, policy=pkg.Policy(tile=9)) == -8
     # LDS of the staged flow does not fit the largest tile
     assert gemm(4, 4, 4, policy=pkg.Policy(flow=pkg.FLOW_STAGED, tile=pkg.TILE_256x128)) == -8
+    # the register-direct flow has no 256x128 tile and needs 16-byte A rows
+    # and, with 64-wide waves, column pairs
+    reg = pkg.FLOW_REG
+    assert gemm(4, 4, 4, policy=pkg.Policy(flow=reg, tile=pkg.TILE_256x128)) == -8
+    assert gemm(4, 4, 6, policy=pkg.Policy(flow=reg, tile=pkg.TILE_64x64)) == -8
+    assert gemm(4, 4, 4, A=PA + 4, policy=pkg.Policy(flow=reg, tile=pkg.TILE_64x64)) == -8
+    assert gemm(4, 5, 4, policy=pkg.Policy(flow=reg, tile=pkg.TILE_128x128)) == -8
+    assert gemm(4, 4, 4, B=PB + 4, policy=pkg.Policy(flow=reg, tile=pkg.TILE_128x128)) == -8
+    assert gemm(4, 4, 4, lda=1 << 23, policy=pkg.Policy(flow=reg, tile=pkg.TILE_64x64)) == -8
 
 
 def test_empty_problems_are_noops():

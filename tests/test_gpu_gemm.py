@@ -1,8 +1,10 @@
 """Parity of the batched emulated SGEMM (Sec. 4.4) against the oracle, through
 the C ABI on the GPU.
 
-* every policy (split flow, direct flow, staged flow; error correction on and
-  off; every tile) on shapes that span several tiles and ragged tails;
+* every policy (split flow, direct flow, staged flow, register-direct flow;
+  error correction on and off; every tile) on shapes that span several
+  tiles and ragged tails, and every k-loop path of the register-direct
+  flow;
 * edge cases: k = 0, empty problems, a single element, broadcast operands
   (zero batch stride), padded leading dimensions, unaligned pointers (the
   scalar-load path);
@@ -33,11 +35,21 @@ POLICIES = [
     pkg.Policy(pkg.FLOW_DIRECT, 1, pkg.TILE_256x128),
     pkg.Policy(pkg.FLOW_STAGED, 1, pkg.TILE_64x64),
     pkg.Policy(pkg.FLOW_STAGED, 1, pkg.TILE_128x128),
+    pkg.Policy(pkg.FLOW_REG, 1, pkg.TILE_64x64),
+    pkg.Policy(pkg.FLOW_REG, 1, pkg.TILE_128x128),
 ]
 
 
 def _pid(p):
     return f"flow{p.flow}-ec{p.ec}-tile{p.tile}"
+
+
+def _reg_supported(policy, k, n):
+    """The register-direct flow needs 16-byte A rows (k a multiple of 4 for a
+    packed operand) and, for its 64-wide waves, column pairs (n even)."""
+    if policy is None or policy.flow != pkg.FLOW_REG:
+        return True
+    return k % 4 == 0 and (policy.tile == pkg.TILE_64x64 or n % 2 == 0)
 
 
 def _run(A, B, policy=None, C=None):
@@ -64,9 +76,67 @@ def test_policies_ragged_shapes(policy, shape):
     batch, m, n, k = shape
     print(f"case policy={_pid(policy)} shape={shape}", flush=True)
     A, B = synth.gemm_inputs(batch, m, n, k, seed=11 + m + n + k)
+    if not _reg_supported(policy, k, n):
+        with pytest.raises(pkg.SgemmEmuError) as ei:
+            _run(A, B, policy)
+        assert ei.value.code == -8
+        return
     C = _run(A, B, policy)
     ref = oracle.gemm(A.numpy(), B.numpy())
     gate(C, ref, k, f"{_pid(policy)} {shape}", max_gate=gate_applies(k, batch * m * n))
+
+
+# Shapes for the register-direct flow: every k-loop path of its register
+# ring (k < 16 D, exactly D steps, steady state, 1 .. D - 1 extra steps, a
+# partial last step), ragged m and n, a wave tile entirely outside C.
+REG_SHAPES = [  # batch, m, n, k
+    (2, 64, 64, 64),
+    (3, 130, 66, 100),
+    (1, 257, 130, 208),
+    (2, 17, 34, 300),
+    (1, 70, 96, 36),
+    (2, 33, 64, 4),
+    (1, 96, 128, 112),
+    (2, 128, 128, 80),
+    (1, 192, 256, 192),
+    (2, 40, 200, 48),
+    (1, 160, 98, 144),
+]
+
+
+@pytest.mark.parametrize("tile", [pkg.TILE_64x64, pkg.TILE_128x128])
+@pytest.mark.parametrize("shape", REG_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_register_direct_flow_shapes(tile, shape):
+    batch, m, n, k = shape
+    policy = pkg.Policy(pkg.FLOW_REG, 1, tile)
+    print(f"case policy={_pid(policy)} shape={shape}", flush=True)
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=31 + m + n + k)
+    C = _run(A, B, policy)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(C, ref, k, f"{_pid(policy)} {shape}", max_gate=gate_applies(k, batch * m * n))
+
+
+def test_register_direct_flow_b_pairs():
+    """B 8-byte but not 16-byte aligned: the 128x128 tile falls back from
+    4-wide to 2-wide B loads (waves of 64 x 64)."""
+    dev = device()
+    A, B = synth.gemm_inputs(2, 96, 132, 72, seed=43)
+    flat = torch.zeros(B.numel() + 2, device=dev)
+    flat[2:] = B.reshape(-1).to(dev)
+    Bd = flat[2:].view(2, 72, 132)
+    C = to_np(pkg.sgemm_emu_batched(A.to(dev), Bd, policy=pkg.Policy(pkg.FLOW_REG, 1,
+                                                                      pkg.TILE_128x128)))
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(C, ref, 72, "reg B pairs")
+
+
+def test_register_direct_flow_odd_columns_32_wide():
+    """32x32 waves load single columns, so an odd n is fine there."""
+    policy = pkg.Policy(pkg.FLOW_REG, 1, pkg.TILE_64x64)
+    A, B = synth.gemm_inputs(2, 75, 77, 68, seed=41)
+    C = _run(A, B, policy)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(C, ref, 68, "reg odd n")
 
 
 @pytest.mark.parametrize("policy", POLICIES, ids=_pid)
@@ -79,7 +149,7 @@ def test_integer_inputs_exact(policy):
     assert np.array_equal(C, ref.astype(np.float32))
 
 
-@pytest.mark.parametrize("flow", [pkg.FLOW_SPLIT, pkg.FLOW_DIRECT, pkg.FLOW_STAGED])
+@pytest.mark.parametrize("flow", [pkg.FLOW_SPLIT, pkg.FLOW_DIRECT, pkg.FLOW_STAGED, pkg.FLOW_REG])
 def test_error_correction_is_live(flow):
     """Without the two correction products the error is at the fp16 level
     (about 2^-11 relative); with them it is at the FP32 level."""
