@@ -5,10 +5,14 @@
                     [--flow F --ec E --tile T] [--no-cpu-baseline]
 
 A step is one sgemm_emu_batched call over the whole batch of the workload
-(every row of the hot path: global->LDS staging, split, three MFMA
-products, combine and store), with inputs already resident in HBM.  The
-default workload is the batched one, 4096 products of 128 x 128 x 128
-(uniform(-1, 1) FP32, seed 2).
+(every step of the path: operand loads, split, three MFMA products, combine
+and store), with inputs already resident in HBM, under the policy the
+library picks for it (or the one given).  The default workload is the
+batched one, 4096 products of 128 x 128 x 128 (uniform(-1, 1) FP32, seed 2).
+
+The roofline's "traffic" is the HBM traffic a counter run measured for this
+workload and kernel (profiles/traffic.json), reported only while the
+kernel's sources are unchanged since that run.
 
 One JSON line is printed with the emulated TFLOP/s, the roofline of the
 dominant kernel (its average duration from HIP events recorded on the stream
@@ -22,6 +26,8 @@ to scale the HBM traffic counters of a profiler run.
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -41,6 +47,53 @@ PEAK_FP16_MFMA_TFLOPS = 2516.6   # dense
 PEAK_FP32_VECTOR_TFLOPS = 157.3
 
 METRIC = "emulated-SGEMM TFLOP/s (batched)"
+
+# HBM traffic measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE), per
+# workload, with the hash of the kernel sources it was taken on
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are added
+    "bgemm_reg_kernel": "bgemm_reg.hip",
+    "bgemm_emu_kernel": "bgemm.hip",
+    "householder64_kernel": "householder.hip",
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """SHA-256 over the sources a kernel is built from: its translation unit
+    and every header."""
+    csrc = os.path.join(ROOT, "paper_2308_15152_amd", "csrc")
+    files = sorted([os.path.join(csrc, KERNEL_SOURCES[kernel])] +
+                   glob.glob(os.path.join(csrc, "*.h*")) +
+                   glob.glob(os.path.join(ROOT, "include", "**", "*.h*"), recursive=True))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.relpath(f, ROOT).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed counter runs, or None if there
+    are none for this workload and kernel or the kernels changed since."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            table = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    e = table.get(workload)
+    if not e or e.get("kernel") != kernel or e.get("source_sha256") != kernel_source_hash(kernel):
+        return None
+    return int(round((e["fetch_kib"] * e["fetch_scale"] + e["write_kib"] * e["write_scale"])
+                     * 1024))
+
+
+def kernel_name(w, resolved) -> str:
+    if w.kind == "householder":
+        return "householder64_kernel"
+    return "bgemm_reg_kernel" if resolved.flow == pkg.FLOW_REG else "bgemm_emu_kernel"
 
 
 def parse():
@@ -152,17 +205,24 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
     dt1 = time.perf_counter() - t0
     n = int(min(w.batch, max(threads, target_s / max(dt1, 1e-4))))
     items = list(range(n))
+    # when the whole batch takes less than the target, time whole passes
+    # until the target is reached
+    reps = 0
     t0 = time.perf_counter()
-    run(items)
-    dt = time.perf_counter() - t0
+    while True:
+        run(items)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if n < w.batch or dt >= target_s:
+            break
     acc_items = items[:min(n, 16)]
     r = ref(acc_items)
     Cs = C_dev[acc_items].cpu().numpy()
     acc = {"max_rel_err_emu": oracle.max_rel_err(Cs, r["c64"], r["n64"]),
            "max_rel_err_fp32": oracle.max_rel_err(r["c32"], r["c64"], r["n64"]),
            "sample": f"items 0..{len(acc_items) - 1}"}
-    sample = f"{n} of {w.batch} batch items"
-    return {"value": per_item * n / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+    sample = f"{n} of {w.batch} batch items" + (f", {reps} passes" if reps > 1 else "")
+    return {"value": per_item * n * reps / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "sample": sample, "seconds": dt}, acc
 
 
@@ -217,8 +277,12 @@ def main():
         roof = {"bound": "hbm", "achieved": bytes_alg / (ms_step * 1e-3) / 1e9,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof["kernel"] = ("householder64_kernel" if w.kind == "householder" else "bgemm_emu_kernel")
+    resolved = None
+    if w.kind == "gemm":
+        A, B = dev_inputs
+        resolved = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
+    roof["kernel"] = kernel_name(w, resolved)
+    roof["traffic"] = measured_traffic(w.name, roof["kernel"])
 
     out = {
         "metric": METRIC,
@@ -235,8 +299,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "kind": w.kind, "batch": w.batch, "m": w.m, "n": w.n,
                    "k": w.k, "dist": w.dist, "seed": w.seed,
-                   "policy": None if policy is None else
-                   {"flow": policy.flow, "ec": policy.ec, "tile": policy.tile}},
+                   "policy": None if resolved is None else
+                   {"flow": resolved.flow, "ec": resolved.ec, "tile": resolved.tile,
+                    "requested": "auto" if policy is None else "explicit"}},
         "frac_fp32_vector_peak": tflops / PEAK_FP32_VECTOR_TFLOPS,
         "frac_fp16_mfma_over_3": tflops / (PEAK_FP16_MFMA_TFLOPS / 3),
         "hbm_GBps_algorithmic": bytes_alg / (ms_step * 1e-3) / 1e9,

@@ -138,6 +138,19 @@ int sgemm_emu_batched_ex(int m, int n, int k,
                          const sgemm_emu_policy_t* policy,
                          hipStream_t stream);
 
+/* The policy sgemm_emu_batched_ex would run for these arguments, with AUTO
+ * flow and tile replaced by the library's choice (ec is copied).  A host-only
+ * query: no HIP call, nothing is enqueued.  Same validation and errors as
+ * sgemm_emu_batched_ex, plus SGEMM_EMU_ERR_NULL for a NULL out; for an
+ * empty problem (nothing would run) out receives the policy unresolved. */
+int sgemm_emu_resolve_policy(int m, int n, int k,
+                             const float* A, int lda,
+                             const float* B, int ldb,
+                             float* C, int ldc,
+                             int batch, sgemm_emu_stride_t stride,
+                             const sgemm_emu_policy_t* policy,
+                             sgemm_emu_policy_t* out);
+
 /*
  * Batched Householder application with the reflector built in registers
  * (Sec. 4.2.1, eq. householder, read as H = I - 2 u u^T):

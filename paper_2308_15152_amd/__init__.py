@@ -18,8 +18,8 @@ import os
 
 __all__ = [
     "SgemmEmuError", "lib_path", "load",
-    "sgemm_emu_batched", "sgemm_emu_batched_ex", "householder_emu_batched",
-    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
+    "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
+    "householder_emu_batched", "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
     "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
     "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128",
@@ -37,8 +37,8 @@ USE_A, USE_B, USE_ACC = 0, 1, 2
 
 # Every symbol declared in include/sgemm_emu.h.
 EXPORTED_SYMBOLS = (
-    "sgemm_emu_batched", "sgemm_emu_batched_ex", "householder_emu_batched",
-    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
+    "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
+    "householder_emu_batched", "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
     "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
 )
 
@@ -88,6 +88,8 @@ def load():
         "sgemm_emu_batched": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride, P], i32),
         "sgemm_emu_batched_ex": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
                                   ctypes.POINTER(Policy), P], i32),
+        "sgemm_emu_resolve_policy": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
+                                      ctypes.POINTER(Policy), ctypes.POINTER(Policy)], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
         "sgemm_emu_split": ([i64, P, P, P, P], i32),
         "mfmae_num_elements": ([i32, i32], i32),
@@ -159,15 +161,9 @@ def _matrix_view(t, name: str):
     return b, rows, cols, ld, t.stride(0) if b > 1 else 0
 
 
-def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None):
-    """C[t] := A[t] @ B[t] with the emulated FP32 product.
-
-    A: [batch, m, k] or [m, k]; B: [batch, k, n] or [k, n] (a 2-D operand is
-    broadcast over the batch); C: [batch, m, n] (allocated if None).  Rows of
-    every operand must be contiguous; leading dimensions and batch strides are
-    taken from the tensors' strides.  Runs on the current torch stream unless
-    ``stream`` (a hipStream_t handle) is given.  With ``policy`` the call goes
-    to sgemm_emu_batched_ex."""
+def _gemm_args(A, B, C):
+    """(m, n, k, lda, ldb, ldc, batch, stride, C) of a batched product; C is
+    allocated if None."""
     import torch
 
     ba, m, k, lda, sa = _matrix_view(A, "A")
@@ -183,6 +179,19 @@ def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None
     if (mc, nc) != (m, n) or (bc if bc is not None else 1) != batch:
         raise ValueError("C has the wrong shape")
     st = Stride(sa, sb, sc if batch > 1 else 0)
+    return m, n, k, lda, ldb, ldc, batch, st, C
+
+
+def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None):
+    """C[t] := A[t] @ B[t] with the emulated FP32 product.
+
+    A: [batch, m, k] or [m, k]; B: [batch, k, n] or [k, n] (a 2-D operand is
+    broadcast over the batch); C: [batch, m, n] (allocated if None).  Rows of
+    every operand must be contiguous; leading dimensions and batch strides are
+    taken from the tensors' strides.  Runs on the current torch stream unless
+    ``stream`` (a hipStream_t handle) is given.  With ``policy`` the call goes
+    to sgemm_emu_batched_ex."""
+    m, n, k, lda, ldb, ldc, batch, st, C = _gemm_args(A, B, C)
     lib = load()
     if policy is None:
         rc = lib.sgemm_emu_batched(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
@@ -193,6 +202,18 @@ def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None
                                       st, ctypes.byref(policy), _stream(stream))
         _check(rc, "sgemm_emu_batched_ex")
     return C
+
+
+def sgemm_emu_resolve_policy(A, B, C, *, policy: Policy | None = None) -> Policy:
+    """The policy the library would run for this product, with AUTO flow and
+    tile resolved (a host-side query; nothing is launched)."""
+    m, n, k, lda, ldb, ldc, batch, st, C = _gemm_args(A, B, C)
+    out = Policy()
+    rc = load().sgemm_emu_resolve_policy(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc,
+                                         batch, st, None if policy is None else
+                                         ctypes.byref(policy), ctypes.byref(out))
+    _check(rc, "sgemm_emu_resolve_policy")
+    return out
 
 
 def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):

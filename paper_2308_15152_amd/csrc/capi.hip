@@ -64,16 +64,19 @@ int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int
     return SGEMM_EMU_OK;
 }
 
-int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
-             int ldc, int batch, sgemm_emu_stride_t st, int flow, int ec, int tile,
-             hipStream_t stream) {
+// Validate, then resolve the policy (flow and tile, AUTO replaced by the
+// library's choice) and fill the kernel arguments.  `launch` is false for an
+// empty problem (nothing to run).
+int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
+                 int ldc, int batch, sgemm_emu_stride_t st, int& flow, int ec, int& tile,
+                 sgemm_emu::GemmArgs& a, bool& launch) {
+    launch = false;
     int rc = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st);
     if (rc != SGEMM_EMU_OK) return rc;
     if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_REG) return SGEMM_EMU_ERR_POLICY;
     if (ec != 0 && ec != 1) return SGEMM_EMU_ERR_POLICY;
     if (tile < SGEMM_EMU_TILE_AUTO || tile > SGEMM_EMU_TILE_256x128) return SGEMM_EMU_ERR_POLICY;
     if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
-    sgemm_emu::GemmArgs a;
     a.m = m;
     a.n = n;
     a.k = k;
@@ -103,14 +106,24 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
         }
     }
     if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
-    hipError_t e;
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
-        e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream);
-    } else {
-        if (!sgemm_emu::gemm_variant_exists(tile, flow)) return SGEMM_EMU_ERR_POLICY;
-        e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
+    } else if (!sgemm_emu::gemm_variant_exists(tile, flow)) {
+        return SGEMM_EMU_ERR_POLICY;
     }
+    launch = true;
+    return SGEMM_EMU_OK;
+}
+
+int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
+             int ldc, int batch, sgemm_emu_stride_t st, int flow, int ec, int tile,
+             hipStream_t stream) {
+    sgemm_emu::GemmArgs a;
+    bool launch;
+    int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st, flow, ec, tile, a, launch);
+    if (rc != SGEMM_EMU_OK || !launch) return rc;
+    hipError_t e = flow == SGEMM_EMU_FLOW_REG ? sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream)
+                                              : sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
@@ -176,6 +189,21 @@ int sgemm_emu_batched_ex(int m, int n, int k, const float* A, int lda, const flo
     if (policy) pol = *policy;
     return run_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, pol.flow, pol.ec, pol.tile,
                     stream);
+}
+
+int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const float* B,
+                             int ldb, float* C, int ldc, int batch, sgemm_emu_stride_t stride,
+                             const sgemm_emu_policy_t* policy, sgemm_emu_policy_t* out) {
+    if (out == nullptr) return SGEMM_EMU_ERR_NULL;
+    sgemm_emu_policy_t pol{SGEMM_EMU_FLOW_AUTO, 1, SGEMM_EMU_TILE_AUTO};
+    if (policy) pol = *policy;
+    sgemm_emu::GemmArgs a;
+    bool launch;
+    int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, pol.flow, pol.ec,
+                          pol.tile, a, launch);
+    if (rc != SGEMM_EMU_OK) return rc;
+    *out = pol;
+    return SGEMM_EMU_OK;
 }
 
 int householder_emu_batched(int n, const float* u, int64_t stride_u, const float* B, int ldb,

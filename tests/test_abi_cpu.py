@@ -111,6 +111,38 @@ def test_policy_values():
     assert gemm(4, 4, 4, lda=1 << 23, policy=pkg.Policy(flow=reg, tile=pkg.TILE_64x64)) == -8
 
 
+def _resolve(m, n, k, batch=1, st=(0, 0, 0), policy=None, A=PA, B=PB, C=PC):
+    lib = pkg.load()
+    out = pkg.Policy()
+    rc = lib.sgemm_emu_resolve_policy(m, n, k, ctypes.c_void_p(A), k, ctypes.c_void_p(B), n,
+                                      ctypes.c_void_p(C), n, batch, S(*st),
+                                      None if policy is None else ctypes.byref(policy),
+                                      ctypes.byref(out))
+    return rc, (out.flow, out.ec, out.tile)
+
+
+def test_resolve_policy():
+    """The automatic choice: the register-direct flow for small products
+    (32 x 32 waves up to 64 x 64, else the 128 x 128 tile), the LDS split
+    flow for large ones; explicit policies pass through; the same
+    validation as the launching entry point."""
+    s128 = 128 * 128
+    assert _resolve(128, 128, 128, 4096, (s128, s128, s128)) == (0, (pkg.FLOW_REG, 1,
+                                                                       pkg.TILE_128x128))
+    assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
+                                                                 pkg.TILE_64x64))
+    assert _resolve(8192, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    # k not a multiple of 4: no 16-byte A rows, so the LDS flow
+    assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
+    pol = pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_64x64)
+    assert _resolve(128, 128, 128, policy=pol) == (0, (pkg.FLOW_DIRECT, 0, pkg.TILE_64x64))
+    assert _resolve(-1, 4, 4)[0] == -1
+    lib = pkg.load()
+    assert lib.sgemm_emu_resolve_policy(4, 4, 4, ctypes.c_void_p(PA), 4, ctypes.c_void_p(PB), 4,
+                                        ctypes.c_void_p(PC), 4, 1, S(0, 0, 0), None,
+                                        None) == -3
+
+
 def test_empty_problems_are_noops():
     assert gemm(0, 4, 4) == 0
     assert gemm(4, 0, 4, ldb=1, ldc=1) == 0
