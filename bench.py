@@ -55,6 +55,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are added
     "bgemm_reg_kernel": "bgemm_reg.hip",
+    "bgemm_big_kernel": "bgemm_big.hip",
     "bgemm_emu_kernel": "bgemm.hip",
     "householder64_kernel": "householder.hip",
 }
@@ -90,10 +91,6 @@ def measured_traffic(workload: str, kernel: str):
                      * 1024))
 
 
-def kernel_name(w, resolved) -> str:
-    if w.kind == "householder":
-        return "householder64_kernel"
-    return "bgemm_reg_kernel" if resolved.flow == pkg.FLOW_REG else "bgemm_emu_kernel"
 
 
 def parse():
@@ -277,11 +274,11 @@ def main():
         roof = {"bound": "hbm", "achieved": bytes_alg / (ms_step * 1e-3) / 1e9,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    resolved = None
+    resolved, kernel = None, "householder64_kernel"
     if w.kind == "gemm":
         A, B = dev_inputs
-        resolved = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
-    roof["kernel"] = kernel_name(w, resolved)
+        resolved, kernel = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
+    roof["kernel"] = kernel
     roof["traffic"] = measured_traffic(w.name, roof["kernel"])
 
     out = {

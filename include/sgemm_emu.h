@@ -139,17 +139,23 @@ int sgemm_emu_batched_ex(int m, int n, int k,
                          hipStream_t stream);
 
 /* The policy sgemm_emu_batched_ex would run for these arguments, with AUTO
- * flow and tile replaced by the library's choice (ec is copied).  A host-only
- * query: no HIP call, nothing is enqueued.  Same validation and errors as
- * sgemm_emu_batched_ex, plus SGEMM_EMU_ERR_NULL for a NULL out; for an
- * empty problem (nothing would run) out receives the policy unresolved. */
+ * flow and tile replaced by the library's choice (ec is copied), and, if
+ * `kernel` is not NULL, the name of the kernel it would launch (a static
+ * string; "" for an empty problem).  A host-only query: no HIP call,
+ * nothing is enqueued.  Same validation and errors as sgemm_emu_batched_ex,
+ * plus SGEMM_EMU_ERR_NULL for a NULL out; for an empty problem (nothing
+ * would run) out receives the policy unresolved.
+ * The split flow with tile 256x128 and error correction runs a pipelined
+ * full-tile kernel when m % 256 == 0, n % 128 == 0, k % 32 == 0, k > 0 and
+ * A and B rows are 16-byte aligned; otherwise the general LDS kernel. */
 int sgemm_emu_resolve_policy(int m, int n, int k,
                              const float* A, int lda,
                              const float* B, int ldb,
                              float* C, int ldc,
                              int batch, sgemm_emu_stride_t stride,
                              const sgemm_emu_policy_t* policy,
-                             sgemm_emu_policy_t* out);
+                             sgemm_emu_policy_t* out,
+                             const char** kernel);
 
 /*
  * Batched Householder application with the reflector built in registers

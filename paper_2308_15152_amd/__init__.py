@@ -89,7 +89,8 @@ def load():
         "sgemm_emu_batched_ex": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
                                   ctypes.POINTER(Policy), P], i32),
         "sgemm_emu_resolve_policy": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
-                                      ctypes.POINTER(Policy), ctypes.POINTER(Policy)], i32),
+                                      ctypes.POINTER(Policy), ctypes.POINTER(Policy),
+                                      ctypes.POINTER(ctypes.c_char_p)], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
         "sgemm_emu_split": ([i64, P, P, P, P], i32),
         "mfmae_num_elements": ([i32, i32], i32),
@@ -204,16 +205,18 @@ def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None
     return C
 
 
-def sgemm_emu_resolve_policy(A, B, C, *, policy: Policy | None = None) -> Policy:
-    """The policy the library would run for this product, with AUTO flow and
-    tile resolved (a host-side query; nothing is launched)."""
+def sgemm_emu_resolve_policy(A, B, C, *, policy: Policy | None = None):
+    """(policy, kernel name) the library would run for this product, with
+    AUTO flow and tile resolved (a host-side query; nothing is launched)."""
     m, n, k, lda, ldb, ldc, batch, st, C = _gemm_args(A, B, C)
     out = Policy()
+    kern = ctypes.c_char_p()
     rc = load().sgemm_emu_resolve_policy(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc,
                                          batch, st, None if policy is None else
-                                         ctypes.byref(policy), ctypes.byref(out))
+                                         ctypes.byref(policy), ctypes.byref(out),
+                                         ctypes.byref(kern))
     _check(rc, "sgemm_emu_resolve_policy")
-    return out
+    return out, (kern.value or b"").decode()
 
 
 def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):

@@ -67,10 +67,21 @@ int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int
 // Validate, then resolve the policy (flow and tile, AUTO replaced by the
 // library's choice) and fill the kernel arguments.  `launch` is false for an
 // empty problem (nothing to run).
+enum Kernel { K_NONE, K_REG, K_BIG, K_LDS };
+
+const char* kernel_name(Kernel k) {
+    switch (k) {
+        case K_REG: return "bgemm_reg_kernel";
+        case K_BIG: return "bgemm_big_kernel";
+        case K_LDS: return "bgemm_emu_kernel";
+        default: return "";
+    }
+}
+
 int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
                  int ldc, int batch, sgemm_emu_stride_t st, int& flow, int ec, int& tile,
-                 sgemm_emu::GemmArgs& a, bool& launch) {
-    launch = false;
+                 sgemm_emu::GemmArgs& a, Kernel& kern) {
+    kern = K_NONE;
     int rc = check_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st);
     if (rc != SGEMM_EMU_OK) return rc;
     if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_REG) return SGEMM_EMU_ERR_POLICY;
@@ -108,10 +119,15 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
+        kern = K_REG;
     } else if (!sgemm_emu::gemm_variant_exists(tile, flow)) {
         return SGEMM_EMU_ERR_POLICY;
+    } else if (flow == SGEMM_EMU_FLOW_SPLIT && tile == SGEMM_EMU_TILE_256x128 &&
+               sgemm_emu::big_supported(a)) {
+        kern = K_BIG;  // full tiles: the pipelined kernel
+    } else {
+        kern = K_LDS;
     }
-    launch = true;
     return SGEMM_EMU_OK;
 }
 
@@ -119,11 +135,18 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
              int ldc, int batch, sgemm_emu_stride_t st, int flow, int ec, int tile,
              hipStream_t stream) {
     sgemm_emu::GemmArgs a;
-    bool launch;
-    int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st, flow, ec, tile, a, launch);
-    if (rc != SGEMM_EMU_OK || !launch) return rc;
-    hipError_t e = flow == SGEMM_EMU_FLOW_REG ? sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream)
-                                              : sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream);
+    Kernel kern;
+    int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, st, flow, ec, tile, a, kern);
+    if (rc != SGEMM_EMU_OK || kern == K_NONE) return rc;
+    hipError_t e;
+    switch (kern) {
+        case K_REG: e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream); break;
+        case K_BIG:
+            e = ec ? sgemm_emu::launch_gemm_big(a, stream)
+                   : sgemm_emu::launch_gemm(a, tile, flow, false, stream);
+            break;
+        default: e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream); break;
+    }
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
@@ -193,16 +216,19 @@ int sgemm_emu_batched_ex(int m, int n, int k, const float* A, int lda, const flo
 
 int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const float* B,
                              int ldb, float* C, int ldc, int batch, sgemm_emu_stride_t stride,
-                             const sgemm_emu_policy_t* policy, sgemm_emu_policy_t* out) {
+                             const sgemm_emu_policy_t* policy, sgemm_emu_policy_t* out,
+                             const char** kernel) {
     if (out == nullptr) return SGEMM_EMU_ERR_NULL;
     sgemm_emu_policy_t pol{SGEMM_EMU_FLOW_AUTO, 1, SGEMM_EMU_TILE_AUTO};
     if (policy) pol = *policy;
     sgemm_emu::GemmArgs a;
-    bool launch;
+    Kernel kern;
     int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, pol.flow, pol.ec,
-                          pol.tile, a, launch);
+                          pol.tile, a, kern);
     if (rc != SGEMM_EMU_OK) return rc;
+    if (kern == K_BIG && pol.ec == 0) kern = K_LDS;
     *out = pol;
+    if (kernel) *kernel = kernel_name(kern);
     return SGEMM_EMU_OK;
 }
 

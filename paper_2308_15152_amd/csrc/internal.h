@@ -31,6 +31,11 @@ bool gemm_variant_exists(int tile, int flow);
 bool reg_flow_supported(const GemmArgs& a, int tile);
 hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t stream);
 
+// Full-tile large-product kernel (split flow, 256 x 128 tiles): true if the
+// shape and alignment allow it.
+bool big_supported(const GemmArgs& a);
+hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t stream);
+
 struct HouseholderArgs {
     int ncols;
     const float* u;

@@ -114,10 +114,12 @@ def test_policy_values():
 def _resolve(m, n, k, batch=1, st=(0, 0, 0), policy=None, A=PA, B=PB, C=PC):
     lib = pkg.load()
     out = pkg.Policy()
+    kern = ctypes.c_char_p()
     rc = lib.sgemm_emu_resolve_policy(m, n, k, ctypes.c_void_p(A), k, ctypes.c_void_p(B), n,
                                       ctypes.c_void_p(C), n, batch, S(*st),
                                       None if policy is None else ctypes.byref(policy),
-                                      ctypes.byref(out))
+                                      ctypes.byref(out), ctypes.byref(kern))
+    _resolve.kernel = (kern.value or b"").decode()
     return rc, (out.flow, out.ec, out.tile)
 
 
@@ -131,7 +133,13 @@ def test_resolve_policy():
                                                                        pkg.TILE_128x128))
     assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
                                                                  pkg.TILE_64x64))
+    assert _resolve(128, 128, 128, 4096, (s128, s128, s128))[0] == 0
+    assert _resolve.kernel == "bgemm_reg_kernel"
     assert _resolve(8192, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_big_kernel"
+    # not a multiple of the full tile: the general LDS kernel
+    assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_emu_kernel"
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
     pol = pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_64x64)
@@ -140,7 +148,7 @@ def test_resolve_policy():
     lib = pkg.load()
     assert lib.sgemm_emu_resolve_policy(4, 4, 4, ctypes.c_void_p(PA), 4, ctypes.c_void_p(PB), 4,
                                         ctypes.c_void_p(PC), 4, 1, S(0, 0, 0), None,
-                                        None) == -3
+                                        None, None) == -3
 
 
 def test_empty_problems_are_noops():

@@ -116,6 +116,47 @@ def test_register_direct_flow_shapes(tile, shape):
     gate(C, ref, k, f"{_pid(policy)} {shape}", max_gate=gate_applies(k, batch * m * n))
 
 
+# Shapes for the pipelined full-tile kernel (split flow, 256 x 128 tiles):
+# one, two, three and five k chunks (every path of its two-stage loop),
+# several tiles and items, padded leading dimensions.
+BIG_SHAPES = [  # batch, m, n, k, pad
+    (1, 256, 128, 32, 0),
+    (2, 256, 256, 64, 0),
+    (1, 512, 384, 96, 0),
+    (3, 256, 128, 160, 4),
+    (1, 768, 256, 320, 8),
+]
+
+
+@pytest.mark.parametrize("shape", BIG_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_full_tile_kernel_shapes(shape):
+    batch, m, n, k, pad = shape
+    dev = device()
+    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128)
+    print(f"case full-tile shape={shape}", flush=True)
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=51 + m + n + k)
+    Ab = torch.zeros((batch, m, k + pad), device=dev)
+    Bb = torch.zeros((batch, k, n + pad), device=dev)
+    Ab[:, :, :k] = A.to(dev)
+    Bb[:, :, :n] = B.to(dev)
+    Ad, Bd = Ab[:, :, :k], Bb[:, :, :n]
+    Cd = torch.empty((batch, m, n), device=dev)
+    _, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, Cd, policy=policy)
+    assert kern == "bgemm_big_kernel"
+    pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=policy)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(to_np(Cd), ref, k, f"full-tile {shape}")
+
+
+def test_full_tile_kernel_integer_exact():
+    g = synth.rng(9)
+    A = synth.integer_matrix((2, 256, 96), g, -8, 8)
+    B = synth.integer_matrix((2, 96, 256), g, -8, 8)
+    C = _run(A, B, pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    ref = np.einsum("bik,bkj->bij", A.numpy().astype(np.int64), B.numpy().astype(np.int64))
+    assert np.array_equal(C, ref.astype(np.float32))
+
+
 def test_register_direct_flow_b_pairs():
     """B 8-byte but not 16-byte aligned: the 128x128 tile falls back from
     4-wide to 2-wide B loads (waves of 64 x 64)."""
