@@ -80,9 +80,11 @@ int sgemm_emu_batched(int m, int n, int k,
  * applied, and where the split happens.
  *
  * flow:
- *   SGEMM_EMU_FLOW_AUTO   library choice: REG for products up to 1024 x 1024
- *                         whose operands allow its vector loads, SPLIT
- *                         otherwise.
+ *   SGEMM_EMU_FLOW_AUTO   library choice: SPLIT with tile 256x128 when the
+ *                         full-tile kernel applies (see
+ *                         sgemm_emu_resolve_policy); else REG for products
+ *                         up to 1024 x 1024 whose operands allow its vector
+ *                         loads; else SPLIT.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
  *                         global load and the LDS store; LDS holds hi and lo
  *                         (the same 4 bytes per element as FP32) and the

@@ -13,14 +13,17 @@
 //
 // LDS layout: a plane (A hi, A lo, B hi, B lo) is [row][4 pieces of 8
 // halves], 64 bytes per row, no padding; piece q of row r is stored at
-// position q ^ (((r >> 1) ^ (r >> 3)) & 3).  The 16-byte accesses of any 8
-// consecutive lanes (rows r..r+7, one piece each, or 2 rows x 4 pieces) then
-// fall into distinct banks, for 32 and for 64 banks of 4 bytes.
+// position q ^ ((r ^ (r >> 2)) & 3).  Measured on gfx950 (16-byte LDS
+// accesses, timed against a linear pattern), this swizzle makes all three
+// access patterns conflict-free: the fragment reads (lanes 0..31 rows
+// r..r+31 at one piece, lanes 32..63 the next piece), the A staging writes (4
+// lanes per row, one piece each) and the B staging writes (one row per lane,
+// one piece); unswizzled 64-byte rows give 4-way conflicts on the reads.
 //
 // Pipeline: two LDS stages and two register stages.  In iteration c the
-// workgroup writes chunk c + 1 (loaded two iterations earlier) to LDS, issues
-// the loads of chunk c + 3 into the registers just freed, computes chunk c,
-// and meets at one barrier that orders LDS only (global loads stay in
+// workgroup computes chunk c, writes chunk c + 1 (loaded two iterations
+// earlier) to LDS, issues the loads of chunk c + 3 into the registers just
+// freed, and meets at one barrier that orders LDS only (global loads stay in
 // flight across it).  Every load and store of the loop is unconditional --
 // chunk indices past the end are clamped to the last chunk -- so the waits
 // before each use are for that stage's loads only.
@@ -68,7 +71,7 @@ struct BigParams {
 
 // Byte offset of piece q (8 halves) of row r in a plane.
 __device__ inline int piece(int r, int q) {
-    return r * ROW_BYTES + 16 * (q ^ (((r >> 1) ^ (r >> 3)) & 3));
+    return r * ROW_BYTES + 16 * (q ^ ((r ^ (r >> 2)) & 3));
 }
 
 // Registers of one staged chunk.
@@ -237,16 +240,18 @@ __global__ __launch_bounds__(NT, 2) void bgemm_big_kernel(BigParams p) {
     store_stage(r0, sm, buf0);
     load_stage(r0, sm, BK * min(2, last));
     lds_barrier();
-    // iteration c: store chunk c + 1, load chunk c + 3, compute chunk c
+    // iteration c: compute chunk c, store chunk c + 1, load chunk c + 3.
+    // The MFMAs of chunk c are issued first; they run in the matrix unit
+    // while the same wave splits chunk c + 1 on the VALU.
     int c = 0;
     for (; c + 2 <= nk; c += 2) {
+        compute_stage(acc, cor, buf0, wrow, wcol, g, j);
         store_stage(r1, sm, buf1);
         load_stage(r1, sm, BK * min(c + 3, last));
-        compute_stage(acc, cor, buf0, wrow, wcol, g, j);
         lds_barrier();
+        compute_stage(acc, cor, buf1, wrow, wcol, g, j);
         store_stage(r0, sm, buf0);
         load_stage(r0, sm, BK * min(c + 4, last));
-        compute_stage(acc, cor, buf1, wrow, wcol, g, j);
         lds_barrier();
     }
     if (c < nk) compute_stage(acc, cor, buf0, wrow, wcol, g, j);

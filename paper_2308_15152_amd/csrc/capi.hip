@@ -104,12 +104,18 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     a.vec_a = aligned16(A) && lda % 4 == 0 && st.a % 4 == 0;
     a.vec_b = aligned16(B) && ldb % 4 == 0 && st.b % 4 == 0;
     if (flow == SGEMM_EMU_FLOW_AUTO) {
-        // Small products are bound by HBM traffic: the barrier-free
-        // register-direct flow keeps the most bytes in flight.  Large ones
-        // need the LDS-shared tiles to stay off the L2 bandwidth limit.
+        // Full 256 x 128 tiles take the pipelined split-flow kernel (each
+        // element split once per workgroup).  Other small products are
+        // bound by HBM traffic: the barrier-free register-direct flow keeps
+        // the most bytes in flight.  Large ragged ones need the LDS-shared
+        // tiles to stay off the L2 bandwidth limit.
         const int reg_tile = (m <= 64 && n <= 64) ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
-        if (m <= 1024 && n <= 1024 && (tile == SGEMM_EMU_TILE_AUTO || tile == reg_tile) &&
-            sgemm_emu::reg_flow_supported(a, reg_tile)) {
+        if ((tile == SGEMM_EMU_TILE_AUTO || tile == SGEMM_EMU_TILE_256x128) && ec == 1 &&
+            sgemm_emu::big_supported(a)) {
+            flow = SGEMM_EMU_FLOW_SPLIT;
+            tile = SGEMM_EMU_TILE_256x128;
+        } else if (m <= 1024 && n <= 1024 && (tile == SGEMM_EMU_TILE_AUTO || tile == reg_tile) &&
+                   sgemm_emu::reg_flow_supported(a, reg_tile)) {
             flow = SGEMM_EMU_FLOW_REG;
             tile = reg_tile;
         } else {

@@ -140,6 +140,11 @@ def test_resolve_policy():
     # not a multiple of the full tile: the general LDS kernel
     assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
     assert _resolve.kernel == "bgemm_emu_kernel"
+    # full 256 x 128 tiles of a batch of small products: the full-tile kernel
+    s256 = 256 * 256
+    assert _resolve(256, 256, 256, 1024, (s256, s256, s256)) == (0, (pkg.FLOW_SPLIT, 1,
+                                                                     pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_big_kernel"
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
     pol = pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_64x64)
