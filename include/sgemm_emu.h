@@ -80,11 +80,13 @@ int sgemm_emu_batched(int m, int n, int k,
  * applied, and where the split happens.
  *
  * flow:
- *   SGEMM_EMU_FLOW_AUTO   library choice: SPLIT with tile 256x128 when the
+ *   SGEMM_EMU_FLOW_AUTO   library choice: SPLIT on full tiles when a
  *                         full-tile kernel applies (see
- *                         sgemm_emu_resolve_policy); else REG for products
- *                         up to 1024 x 1024 whose operands allow its vector
- *                         loads; else SPLIT.
+ *                         sgemm_emu_resolve_policy): 128x256 for products
+ *                         of at least 2048 x 2048, else 256x128, else
+ *                         128x128; otherwise REG for products up to
+ *                         1024 x 1024 whose operands allow its vector loads;
+ *                         otherwise SPLIT.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
  *                         global load and the LDS store; LDS holds hi and lo
  *                         (the same 4 bytes per element as FP32) and the
@@ -123,6 +125,8 @@ int sgemm_emu_batched(int m, int n, int k,
 #define SGEMM_EMU_TILE_64x64 1   /* 4 waves of 32x32 (LDS flows: k-chunk 32) */
 #define SGEMM_EMU_TILE_128x128 2 /* 4 waves of 64x64 (LDS flows: k-chunk 32) */
 #define SGEMM_EMU_TILE_256x128 3 /* 8 waves of 64x64, k-chunk 32; LDS flows  */
+#define SGEMM_EMU_TILE_128x256 4 /* 8 waves of 64x64, k-chunk 32; split flow,
+                                    full tiles only                          */
 
 typedef struct {
     int flow;
@@ -147,9 +151,11 @@ int sgemm_emu_batched_ex(int m, int n, int k,
  * nothing is enqueued.  Same validation and errors as sgemm_emu_batched_ex,
  * plus SGEMM_EMU_ERR_NULL for a NULL out; for an empty problem (nothing
  * would run) out receives the policy unresolved.
- * The split flow with tile 256x128 and error correction runs a pipelined
- * full-tile kernel when m % 256 == 0, n % 128 == 0, k % 32 == 0, k > 0 and
- * A and B rows are 16-byte aligned; otherwise the general LDS kernel. */
+ * The split flow with error correction and tile 128x128, 256x128 or
+ * 128x256 runs a pipelined full-tile kernel when m and n are multiples of
+ * the tile, k is a positive multiple of 32 and A and B rows are 16-byte
+ * aligned; otherwise the general LDS kernel (128x256 has none:
+ * SGEMM_EMU_ERR_POLICY). */
 int sgemm_emu_resolve_policy(int m, int n, int k,
                              const float* A, int lda,
                              const float* B, int ldb,

@@ -22,7 +22,7 @@ __all__ = [
     "householder_emu_batched", "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
     "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
-    "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128",
+    "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128", "TILE_128x256",
     "SHAPE_16x16x32", "SHAPE_32x32x16", "USE_A", "USE_B", "USE_ACC",
     "EXPORTED_SYMBOLS",
 ]
@@ -31,7 +31,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_NAME = "libsgemm_emu.so"
 
 FLOW_AUTO, FLOW_SPLIT, FLOW_DIRECT, FLOW_STAGED, FLOW_REG = 0, 1, 2, 3, 4
-TILE_AUTO, TILE_64x64, TILE_128x128, TILE_256x128 = 0, 1, 2, 3
+TILE_AUTO, TILE_64x64, TILE_128x128, TILE_256x128, TILE_128x256 = 0, 1, 2, 3, 4
 SHAPE_16x16x32, SHAPE_32x32x16 = 0, 1
 USE_A, USE_B, USE_ACC = 0, 1, 2
 

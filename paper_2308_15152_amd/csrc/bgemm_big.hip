@@ -1,12 +1,12 @@
-// Emulated SGEMM for large products (Sec. 4.4): full 256 x 128 tiles of C,
-// split once per workgroup at staging, hi/lo planes in LDS.
+// Emulated SGEMM on full tiles of C (Sec. 4.4): split once per workgroup at
+// staging, hi/lo planes in LDS.
 //
-// Per k chunk of 32, every thread loads 24 FP32 operand elements from global
-// memory into registers (A: two runs of 8 consecutive k of one row; B: 8
-// consecutive k of one column, one 256-byte row segment per wave and load),
+// Per k chunk of 32, every thread loads runs of 8 consecutive k of the
+// operands from global memory into registers (A: 8 consecutive floats of one
+// row; B: 8 rows of one column, one 256-byte row segment per wave and load),
 // splits them there and writes 16-byte hi and lo pieces to LDS, so each
 // element is split once per workgroup and LDS holds 2 + 2 bytes per element,
-// the footprint of the FP32 data.  Eight waves of 64 x 64 read their operand
+// the footprint of the FP32 data.  Waves of 64 x 64 read their operand
 // vectors with one 16-byte LDS read per fragment and run 3 MFMAs per 32 x 32
 // block and 16-wide k step (v_mfma_f32_32x32x16_f16), main and correction
 // products in separate accumulators.
@@ -28,8 +28,9 @@
 // chunk indices past the end are clamped to the last chunk -- so the waits
 // before each use are for that stage's loads only.
 //
-// Only full tiles: m % 256 == 0, n % 128 == 0, k % 32 == 0, 16-byte aligned
-// rows; other shapes take the general LDS kernel.
+// Only full tiles (m and n multiples of the tile, k of 32) with 16-byte
+// aligned rows; other shapes take the general LDS kernel or the
+// register-direct flow.
 #include "internal.h"
 #include "mfmae/frag.hpp"
 #include "mfmae/tcec.hpp"
@@ -45,16 +46,30 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 256, BN = 128, BK = 32;
-constexpr int WM = 64, WN = 64, WAVES_N = BN / WN;
-constexpr int NT = 512;  // 8 waves, two per SIMD
-constexpr int TM = WM / 32, TN = WN / 32;
-constexpr int ROW_BYTES = 2 * BK;  // one row of a binary16 plane
-constexpr int A_PLANE = BM * ROW_BYTES;
-constexpr int B_PLANE = BN * ROW_BYTES;
-constexpr int STAGE_BYTES = 2 * A_PLANE + 2 * B_PLANE;  // 48 KiB
-constexpr int LDS_BYTES = 2 * STAGE_BYTES;              // 96 KiB
-constexpr int A_UNITS = BM * (BK / 8) / NT;             // 8-element A runs per thread: 2
+// Tile configuration: BM x BN workgroup tile, WAVES_M x WAVES_N waves of
+// WM x WN (made of 32 x 32 blocks), W waves per SIMD.
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int W_, int VALU_PER_MFMA_ = 0>
+struct BigCfg {
+    static constexpr int BM = BM_, BN = BN_, BK = 32;
+    static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, W = W_;
+    // 0: compiler's own schedule; else the MFMAs of a chunk are interleaved
+    // with this many VALU instructions each (the split of the next chunk)
+    static constexpr int VALU_PER_MFMA = VALU_PER_MFMA_;
+    static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    static constexpr int NT = 64 * WAVES_M * WAVES_N;
+    static constexpr int TM = WM / 32, TN = WN / 32;
+    static constexpr int ROW_BYTES = 2 * BK;  // one row of a binary16 plane
+    static constexpr int A_PLANE = BM * ROW_BYTES;
+    static constexpr int B_PLANE = BN * ROW_BYTES;
+    static constexpr int STAGE_BYTES = 2 * A_PLANE + 2 * B_PLANE;
+    static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+    // staging units: 8 consecutive k of one A row or one B column
+    static constexpr int A_UNITS = BM * (BK / 8) / NT;
+    static constexpr int B_UNITS = BN * (BK / 8) / NT;
+    static_assert(A_UNITS * NT == BM * (BK / 8) && B_UNITS * NT == BN * (BK / 8), "staging");
+    static_assert(WM % 32 == 0 && WN % 32 == 0, "blocks");
+    static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");
+};
 
 struct BigParams {
     int k;
@@ -69,45 +84,53 @@ struct BigParams {
     int item0;
 };
 
-// Byte offset of piece q (8 halves) of row r in a plane.
+// Byte offset of piece q (8 halves) of row r in a plane of 64-byte rows.
 __device__ inline int piece(int r, int q) {
-    return r * ROW_BYTES + 16 * (q ^ ((r ^ (r >> 2)) & 3));
+    return r * 64 + 16 * (q ^ ((r ^ (r >> 2)) & 3));
 }
 
 // Registers of one staged chunk.
+template <class CF>
 struct Stage {
-    f32x4 a[A_UNITS][2];
-    float b[8];
+    f32x4 a[CF::A_UNITS][2];
+    float b[CF::B_UNITS][8];
 };
 
 // Per-thread staging coordinates (constant over the k loop).
+template <class CF>
 struct StageMap {
-    const float* a[A_UNITS];  // A[m0 + row][8 q]
-    const float* b;           // B[8 kg][n0 + n]
+    const float* a[CF::A_UNITS];  // A[m0 + row][8 q]
+    const float* b[CF::B_UNITS];  // B[8 kg][n0 + n]
     int64_t ldb;
-    int a_lds[A_UNITS];       // piece(row, q)
-    int b_lds;                // piece(n, kg)
+    int a_lds[CF::A_UNITS];       // piece(row, q)
+    int b_lds[CF::B_UNITS];       // piece(n, kg)
 };
 
-__device__ inline void load_stage(Stage& st, const StageMap& sm, int k0) {
+template <class CF>
+__device__ inline void load_stage(Stage<CF>& st, const StageMap<CF>& sm, int k0) {
 #pragma unroll
-    for (int u = 0; u < A_UNITS; ++u) {
+    for (int u = 0; u < CF::A_UNITS; ++u) {
         st.a[u][0] = *reinterpret_cast<const f32x4*>(sm.a[u] + k0);
         st.a[u][1] = *reinterpret_cast<const f32x4*>(sm.a[u] + k0 + 4);
     }
-    const float* bp = sm.b + (int64_t)k0 * sm.ldb;
 #pragma unroll
-    for (int v = 0; v < 8; ++v) st.b[v] = bp[(int64_t)v * sm.ldb];
+    for (int u = 0; u < CF::B_UNITS; ++u) {
+        const float* bp = sm.b[u] + (int64_t)k0 * sm.ldb;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) st.b[u][v] = bp[(int64_t)v * sm.ldb];
+    }
 }
 
 // Split the staged chunk and write its hi and lo pieces to LDS stage `buf`.
-__device__ inline void store_stage(const Stage& st, const StageMap& sm, unsigned char* buf) {
+template <class CF>
+__device__ inline void store_stage(const Stage<CF>& st, const StageMap<CF>& sm,
+                                   unsigned char* buf) {
     unsigned char* a_hi = buf;
-    unsigned char* a_lo = buf + A_PLANE;
-    unsigned char* b_hi = buf + 2 * A_PLANE;
-    unsigned char* b_lo = b_hi + B_PLANE;
+    unsigned char* a_lo = buf + CF::A_PLANE;
+    unsigned char* b_hi = buf + 2 * CF::A_PLANE;
+    unsigned char* b_lo = b_hi + CF::B_PLANE;
 #pragma unroll
-    for (int u = 0; u < A_UNITS; ++u) {
+    for (int u = 0; u < CF::A_UNITS; ++u) {
         const float x[8] = {st.a[u][0][0], st.a[u][0][1], st.a[u][0][2], st.a[u][0][3],
                             st.a[u][1][0], st.a[u][1][1], st.a[u][1][2], st.a[u][1][3]};
         half8_t hi, lo;
@@ -115,53 +138,71 @@ __device__ inline void store_stage(const Stage& st, const StageMap& sm, unsigned
         *reinterpret_cast<half8_t*>(a_hi + sm.a_lds[u]) = hi;
         *reinterpret_cast<half8_t*>(a_lo + sm.a_lds[u]) = lo;
     }
-    half8_t hi, lo;
-    mfmae::tcec::split8(st.b, hi, lo);
-    *reinterpret_cast<half8_t*>(b_hi + sm.b_lds) = hi;
-    *reinterpret_cast<half8_t*>(b_lo + sm.b_lds) = lo;
+#pragma unroll
+    for (int u = 0; u < CF::B_UNITS; ++u) {
+        half8_t hi, lo;
+        mfmae::tcec::split8(st.b[u], hi, lo);
+        *reinterpret_cast<half8_t*>(b_hi + sm.b_lds[u]) = hi;
+        *reinterpret_cast<half8_t*>(b_lo + sm.b_lds[u]) = lo;
+    }
 }
 
 // Both 16-wide k steps of one chunk from LDS stage `buf`.
-__device__ inline void compute_stage(f32x16_t (&acc)[TM][TN], f32x16_t (&cor)[TM][TN],
-                                     const unsigned char* buf, int wrow, int wcol, int g, int j) {
+template <class CF>
+__device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
+                                     f32x16_t (&cor)[CF::TM][CF::TN], const unsigned char* buf,
+                                     int wrow, int wcol, int g, int j) {
     const unsigned char* a_hi = buf;
-    const unsigned char* a_lo = buf + A_PLANE;
-    const unsigned char* b_hi = buf + 2 * A_PLANE;
-    const unsigned char* b_lo = b_hi + B_PLANE;
+    const unsigned char* a_lo = buf + CF::A_PLANE;
+    const unsigned char* b_hi = buf + 2 * CF::A_PLANE;
+    const unsigned char* b_lo = b_hi + CF::B_PLANE;
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
+    for (int s = 0; s < CF::BK / 16; ++s) {
         const int q = 2 * s + g;  // k = 16 s + 8 g + (0..7), the same for A and B
-        half8_t ahi[TM], alo[TM], bhi[TN], blo[TN];
+        half8_t ahi[CF::TM], alo[CF::TM], bhi[CF::TN], blo[CF::TN];
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm) {
+        for (int tm = 0; tm < CF::TM; ++tm) {
             const int o = piece(wrow + 32 * tm + j, q);
             ahi[tm] = *reinterpret_cast<const half8_t*>(a_hi + o);
             alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
         }
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
+        for (int tn = 0; tn < CF::TN; ++tn) {
             const int o = piece(wcol + 32 * tn + j, q);
             bhi[tn] = *reinterpret_cast<const half8_t*>(b_hi + o);
             blo[tn] = *reinterpret_cast<const half8_t*>(b_lo + o);
         }
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
+        for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
-            for (int tn = 0; tn < TN; ++tn)
+            for (int tn = 0; tn < CF::TN; ++tn)
                 acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[tm], bhi[tn], acc[tm][tn],
                                                                      0, 0, 0);
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
+        for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
-            for (int tn = 0; tn < TN; ++tn)
+            for (int tn = 0; tn < CF::TN; ++tn)
                 cor[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(alo[tm], bhi[tn], cor[tm][tn],
                                                                      0, 0, 0);
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
+        for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
-            for (int tn = 0; tn < TN; ++tn)
+            for (int tn = 0; tn < CF::TN; ++tn)
                 cor[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[tm], blo[tn], cor[tm][tn],
                                                                      0, 0, 0);
+    }
+}
+
+// Ask the scheduler to interleave the chunk's MFMAs with the VALU work of
+// the split, so one wave issues both while the matrix unit is busy.
+template <class CF>
+__device__ inline void interleave() {
+    if constexpr (CF::VALU_PER_MFMA > 0) {
+#pragma unroll
+        for (int i = 0; i < 3 * (CF::BK / 16) * CF::TM * CF::TN; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, CF::VALU_PER_MFMA, 0);  // VALU
+        }
     }
 }
 
@@ -173,8 +214,9 @@ __device__ inline void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-__global__ __launch_bounds__(NT, 2) void bgemm_big_kernel(BigParams p) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+template <class CF>
+__global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[CF::LDS_BYTES];
 
     const int task = xcd_task(blockIdx.x, gridDim.x);
     if (task >= p.ntasks) return;  // the whole workgroup leaves together
@@ -189,8 +231,8 @@ __global__ __launch_bounds__(NT, 2) void bgemm_big_kernel(BigParams p) {
     const int first_m = grp * GROUP_M;
     const int gm = min(p.tiles_m - first_m, GROUP_M);
     const int r = t - grp * group_size;
-    const int m0 = (first_m + r % gm) * BM;
-    const int n0 = (r / gm) * BN;
+    const int m0 = (first_m + r % gm) * CF::BM;
+    const int n0 = (r / gm) * CF::BN;
 
     const int64_t it = (int64_t)item + p.item0;
     const float* __restrict__ Ab = p.A + it * p.sa;
@@ -198,71 +240,76 @@ __global__ __launch_bounds__(NT, 2) void bgemm_big_kernel(BigParams p) {
     float* __restrict__ Cb = p.C + it * p.sc;
 
     const int tid = threadIdx.x;
-    StageMap sm;
+    StageMap<CF> sm;
 #pragma unroll
-    for (int u = 0; u < A_UNITS; ++u) {
-        const int unit = u * NT + tid;
+    for (int u = 0; u < CF::A_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
         const int row = unit >> 2, q = unit & 3;
         sm.a[u] = Ab + (int64_t)(m0 + row) * p.lda + 8 * q;
         sm.a_lds[u] = piece(row, q);
     }
-    {
-        const int n = tid & (BN - 1), kg = tid / BN;
-        sm.b = Bb + (int64_t)(8 * kg) * p.ldb + n0 + n;
-        sm.ldb = p.ldb;
-        sm.b_lds = piece(n, kg);
+#pragma unroll
+    for (int u = 0; u < CF::B_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
+        const int n = unit % CF::BN, kg = unit / CF::BN;
+        sm.b[u] = Bb + (int64_t)(8 * kg) * p.ldb + n0 + n;
+        sm.b_lds[u] = piece(n, kg);
     }
+    sm.ldb = p.ldb;
 
     const int wave = tid >> 6;
     const int l = tid & 63;
     const int g = l >> 5, j = l & 31;
-    const int wrow = (wave / WAVES_N) * WM;
-    const int wcol = (wave % WAVES_N) * WN;
+    const int wrow = (wave / CF::WAVES_N) * CF::WM;
+    const int wcol = (wave % CF::WAVES_N) * CF::WN;
 
-    f32x16_t acc[TM][TN], cor[TM][TN];
+    f32x16_t acc[CF::TM][CF::TN], cor[CF::TM][CF::TN];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+    for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
+        for (int tn = 0; tn < CF::TN; ++tn)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 acc[tm][tn][e] = 0.0f;
                 cor[tm][tn][e] = 0.0f;
             }
 
-    const int nk = p.k / BK;  // >= 1
+    const int nk = p.k / CF::BK;  // >= 1
     const int last = nk - 1;
     unsigned char* buf0 = smem;
-    unsigned char* buf1 = smem + STAGE_BYTES;
-    Stage r0, r1;
-    load_stage(r0, sm, 0);
-    load_stage(r1, sm, BK * min(1, last));
-    store_stage(r0, sm, buf0);
-    load_stage(r0, sm, BK * min(2, last));
+    unsigned char* buf1 = smem + CF::STAGE_BYTES;
+    Stage<CF> r0, r1;
+    load_stage<CF>(r0, sm, 0);
+    load_stage<CF>(r1, sm, CF::BK * min(1, last));
+    store_stage<CF>(r0, sm, buf0);
+    load_stage<CF>(r0, sm, CF::BK * min(2, last));
     lds_barrier();
     // iteration c: compute chunk c, store chunk c + 1, load chunk c + 3.
     // The MFMAs of chunk c are issued first; they run in the matrix unit
     // while the same wave splits chunk c + 1 on the VALU.
     int c = 0;
     for (; c + 2 <= nk; c += 2) {
-        compute_stage(acc, cor, buf0, wrow, wcol, g, j);
-        store_stage(r1, sm, buf1);
-        load_stage(r1, sm, BK * min(c + 3, last));
+        compute_stage<CF>(acc, cor, buf0, wrow, wcol, g, j);
+        store_stage<CF>(r1, sm, buf1);
+        load_stage<CF>(r1, sm, CF::BK * min(c + 3, last));
+        interleave<CF>();
         lds_barrier();
-        compute_stage(acc, cor, buf1, wrow, wcol, g, j);
-        store_stage(r0, sm, buf0);
-        load_stage(r0, sm, BK * min(c + 4, last));
+        compute_stage<CF>(acc, cor, buf1, wrow, wcol, g, j);
+        store_stage<CF>(r0, sm, buf0);
+        load_stage<CF>(r0, sm, CF::BK * min(c + 4, last));
+        interleave<CF>();
         lds_barrier();
     }
-    if (c < nk) compute_stage(acc, cor, buf0, wrow, wcol, g, j);
+    if (c < nk) compute_stage<CF>(acc, cor, buf0, wrow, wcol, g, j);
 
     // Epilogue: C = main + corr * 2^-11.  Element e of a 32 x 32 block is
     // row 8 (e / 4) + 4 g + e % 4, column j.
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+    for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-            float* cp = Cb + (int64_t)(m0 + wrow + 32 * tm + 4 * g) * p.ldc + n0 + wcol + 32 * tn + j;
+        for (int tn = 0; tn < CF::TN; ++tn) {
+            float* cp = Cb + (int64_t)(m0 + wrow + 32 * tm + 4 * g) * p.ldc + n0 + wcol +
+                        32 * tn + j;
 #pragma unroll
             for (int e = 0; e < 16; ++e)
                 cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc] =
@@ -270,14 +317,8 @@ __global__ __launch_bounds__(NT, 2) void bgemm_big_kernel(BigParams p) {
         }
 }
 
-}  // namespace
-
-bool big_supported(const GemmArgs& a) {
-    return a.m % BM == 0 && a.n % BN == 0 && a.k % BK == 0 && a.k > 0 && a.vec_a && a.vec_b;
-}
-
-hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t stream) {
-    if (!big_supported(a)) return hipErrorInvalidValue;
+template <class CF>
+hipError_t launch_big_cfg(const GemmArgs& a, hipStream_t stream) {
     BigParams p;
     p.k = a.k;
     p.A = a.A;
@@ -289,22 +330,57 @@ hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t stream) {
     p.C = a.C;
     p.ldc = a.ldc;
     p.sc = a.sc;
-    p.tiles_m = a.m / BM;
-    p.tiles_n = a.n / BN;
+    p.tiles_m = a.m / CF::BM;
+    p.tiles_n = a.n / CF::BN;
     const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
     // one launch stays below 2^31 work-items
-    const int64_t max_tasks = (int64_t(1) << 31) / NT - 1;
+    const int64_t max_tasks = (int64_t(1) << 31) / CF::NT - 1;
     if (tiles > max_tasks) return hipErrorInvalidConfiguration;
     const int64_t items_per_launch = max_tasks / tiles;
     for (int64_t i0 = 0; i0 < a.batch; i0 += items_per_launch) {
         const int64_t items = a.batch - i0 < items_per_launch ? a.batch - i0 : items_per_launch;
         p.ntasks = (int)(items * tiles);
         p.item0 = (int)i0;
-        hipLaunchKernelGGL(bgemm_big_kernel, dim3((unsigned)p.ntasks), dim3(NT), 0, stream, p);
+        hipLaunchKernelGGL(bgemm_big_kernel<CF>, dim3((unsigned)p.ntasks), dim3(CF::NT), 0, stream,
+                           p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// The three full-tile configurations.  128 x 256 (eight 64 x 64 waves, the
+// MFMAs of a chunk interleaved with four VALU instructions each) for large
+// products; 256 x 128 for batches of 256-row products; 128 x 128 (four
+// 64 x 64 waves, two workgroups per CU) for batches of 128-row products.
+using Big128x256 = BigCfg<128, 256, 2, 4, 2, 4>;
+using Big256x128 = BigCfg<256, 128, 4, 2, 2>;
+using Big128x128 = BigCfg<128, 128, 2, 2, 2>;
+
+template <class CF>
+bool fits(const GemmArgs& a) {
+    return a.m % CF::BM == 0 && a.n % CF::BN == 0 && a.k % CF::BK == 0 && a.k > 0 && a.vec_a &&
+           a.vec_b;
+}
+
+}  // namespace
+
+bool big_supported(const GemmArgs& a, int tile) {
+    switch (tile) {
+        case SGEMM_EMU_TILE_128x128: return fits<Big128x128>(a);
+        case SGEMM_EMU_TILE_256x128: return fits<Big256x128>(a);
+        case SGEMM_EMU_TILE_128x256: return fits<Big128x256>(a);
+        default: return false;
+    }
+}
+
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, hipStream_t stream) {
+    if (!big_supported(a, tile)) return hipErrorInvalidValue;
+    switch (tile) {
+        case SGEMM_EMU_TILE_128x128: return launch_big_cfg<Big128x128>(a, stream);
+        case SGEMM_EMU_TILE_256x128: return launch_big_cfg<Big256x128>(a, stream);
+        default: return launch_big_cfg<Big128x256>(a, stream);
+    }
 }
 
 }  // namespace sgemm_emu

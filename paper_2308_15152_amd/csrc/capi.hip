@@ -86,7 +86,7 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     if (rc != SGEMM_EMU_OK) return rc;
     if (flow < SGEMM_EMU_FLOW_AUTO || flow > SGEMM_EMU_FLOW_REG) return SGEMM_EMU_ERR_POLICY;
     if (ec != 0 && ec != 1) return SGEMM_EMU_ERR_POLICY;
-    if (tile < SGEMM_EMU_TILE_AUTO || tile > SGEMM_EMU_TILE_256x128) return SGEMM_EMU_ERR_POLICY;
+    if (tile < SGEMM_EMU_TILE_AUTO || tile > SGEMM_EMU_TILE_128x256) return SGEMM_EMU_ERR_POLICY;
     if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
     a.m = m;
     a.n = n;
@@ -110,10 +110,19 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
         // the most bytes in flight.  Large ragged ones need the LDS-shared
         // tiles to stay off the L2 bandwidth limit.
         const int reg_tile = (m <= 64 && n <= 64) ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
-        if ((tile == SGEMM_EMU_TILE_AUTO || tile == SGEMM_EMU_TILE_256x128) && ec == 1 &&
-            sgemm_emu::big_supported(a)) {
+        int big_tile = SGEMM_EMU_TILE_AUTO;
+        if (ec == 1) {
+            const int order[3] = {(int64_t)m * n >= 2048 * 2048 ? SGEMM_EMU_TILE_128x256
+                                                                 : SGEMM_EMU_TILE_256x128,
+                                  SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
+            for (int t : order)
+                if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&
+                    sgemm_emu::big_supported(a, t))
+                    big_tile = t;
+        }
+        if (big_tile != SGEMM_EMU_TILE_AUTO) {
             flow = SGEMM_EMU_FLOW_SPLIT;
-            tile = SGEMM_EMU_TILE_256x128;
+            tile = big_tile;
         } else if (m <= 1024 && n <= 1024 && (tile == SGEMM_EMU_TILE_AUTO || tile == reg_tile) &&
                    sgemm_emu::reg_flow_supported(a, reg_tile)) {
             flow = SGEMM_EMU_FLOW_REG;
@@ -126,13 +135,12 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
         kern = K_REG;
-    } else if (!sgemm_emu::gemm_variant_exists(tile, flow)) {
-        return SGEMM_EMU_ERR_POLICY;
-    } else if (flow == SGEMM_EMU_FLOW_SPLIT && tile == SGEMM_EMU_TILE_256x128 &&
-               sgemm_emu::big_supported(a)) {
+    } else if (flow == SGEMM_EMU_FLOW_SPLIT && ec == 1 && sgemm_emu::big_supported(a, tile)) {
         kern = K_BIG;  // full tiles: the pipelined kernel
-    } else {
+    } else if (tile != SGEMM_EMU_TILE_128x256 && sgemm_emu::gemm_variant_exists(tile, flow)) {
         kern = K_LDS;
+    } else {
+        return SGEMM_EMU_ERR_POLICY;
     }
     return SGEMM_EMU_OK;
 }
@@ -147,10 +155,7 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
     hipError_t e;
     switch (kern) {
         case K_REG: e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream); break;
-        case K_BIG:
-            e = ec ? sgemm_emu::launch_gemm_big(a, stream)
-                   : sgemm_emu::launch_gemm(a, tile, flow, false, stream);
-            break;
+        case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, stream); break;
         default: e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream); break;
     }
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
@@ -232,7 +237,6 @@ int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const
     int rc = resolve_gemm(m, n, k, A, lda, B, ldb, C, ldc, batch, stride, pol.flow, pol.ec,
                           pol.tile, a, kern);
     if (rc != SGEMM_EMU_OK) return rc;
-    if (kern == K_BIG && pol.ec == 0) kern = K_LDS;
     *out = pol;
     if (kernel) *kernel = kernel_name(kern);
     return SGEMM_EMU_OK;

@@ -31,10 +31,10 @@ bool gemm_variant_exists(int tile, int flow);
 bool reg_flow_supported(const GemmArgs& a, int tile);
 hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t stream);
 
-// Full-tile large-product kernel (split flow, 256 x 128 tiles): true if the
-// shape and alignment allow it.
-bool big_supported(const GemmArgs& a);
-hipError_t launch_gemm_big(const GemmArgs& a, hipStream_t stream);
+// Pipelined full-tile kernels (split flow; tiles 128x128, 256x128,
+// 128x256): true if the shape and alignment allow the tile.
+bool big_supported(const GemmArgs& a, int tile);
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, hipStream_t stream);
 
 struct HouseholderArgs {
     int ncols;

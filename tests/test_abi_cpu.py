@@ -124,31 +124,45 @@ def _resolve(m, n, k, batch=1, st=(0, 0, 0), policy=None, A=PA, B=PB, C=PC):
 
 
 def test_resolve_policy():
-    """The automatic choice: the register-direct flow for small products
-    (32 x 32 waves up to 64 x 64, else the 128 x 128 tile), the LDS split
-    flow for large ones; explicit policies pass through; the same
-    validation as the launching entry point."""
+    """The automatic choice: the pipelined full-tile kernel whenever a tile
+    fits (128 x 256 for large products, else 256 x 128, else 128 x 128), the
+    register-direct flow for other small products (32 x 32 waves up to
+    64 x 64), the general LDS split flow otherwise; explicit policies pass
+    through; the same validation as the launching entry point."""
     s128 = 128 * 128
-    assert _resolve(128, 128, 128, 4096, (s128, s128, s128)) == (0, (pkg.FLOW_REG, 1,
+    assert _resolve(128, 128, 128, 4096, (s128, s128, s128)) == (0, (pkg.FLOW_SPLIT, 1,
                                                                        pkg.TILE_128x128))
-    assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
-                                                                 pkg.TILE_64x64))
-    assert _resolve(128, 128, 128, 4096, (s128, s128, s128))[0] == 0
-    assert _resolve.kernel == "bgemm_reg_kernel"
-    assert _resolve(8192, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
     assert _resolve.kernel == "bgemm_big_kernel"
-    # not a multiple of the full tile: the general LDS kernel
-    assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
-    assert _resolve.kernel == "bgemm_emu_kernel"
-    # full 256 x 128 tiles of a batch of small products: the full-tile kernel
     s256 = 256 * 256
     assert _resolve(256, 256, 256, 1024, (s256, s256, s256)) == (0, (pkg.FLOW_SPLIT, 1,
                                                                      pkg.TILE_256x128))
     assert _resolve.kernel == "bgemm_big_kernel"
+    assert _resolve(8192, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
+    assert _resolve.kernel == "bgemm_big_kernel"
+    assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
+                                                                 pkg.TILE_64x64))
+    assert _resolve.kernel == "bgemm_reg_kernel"
+    # ragged small products: register-direct 128x128
+    assert _resolve(130, 132, 100, 8, (130 * 100, 100 * 132, 130 * 132)) == (
+        0, (pkg.FLOW_REG, 1, pkg.TILE_128x128))
+    # not a multiple of any full tile and large: the general LDS kernel
+    assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_emu_kernel"
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
+    assert _resolve.kernel == "bgemm_emu_kernel"
     pol = pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_64x64)
     assert _resolve(128, 128, 128, policy=pol) == (0, (pkg.FLOW_DIRECT, 0, pkg.TILE_64x64))
+    # the 128x256 tile exists only for full tiles of the split flow
+    assert _resolve(128, 256, 64, policy=pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))[0] == 0
+    assert _resolve(128, 200, 64, policy=pkg.Policy(pkg.FLOW_SPLIT, 1,
+                                                    pkg.TILE_128x256))[0] == -8
+    assert _resolve(128, 256, 64, policy=pkg.Policy(pkg.FLOW_DIRECT, 1,
+                                                    pkg.TILE_128x256))[0] == -8
+    # without error correction the full-tile kernel is not used
+    assert _resolve(256, 256, 256, policy=pkg.Policy(pkg.FLOW_SPLIT, 0,
+                                                     pkg.TILE_256x128))[0] == 0
+    assert _resolve.kernel == "bgemm_emu_kernel"
     assert _resolve(-1, 4, 4)[0] == -1
     lib = pkg.load()
     assert lib.sgemm_emu_resolve_policy(4, 4, 4, ctypes.c_void_p(PA), 4, ctypes.c_void_p(PB), 4,

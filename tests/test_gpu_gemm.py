@@ -116,24 +116,27 @@ def test_register_direct_flow_shapes(tile, shape):
     gate(C, ref, k, f"{_pid(policy)} {shape}", max_gate=gate_applies(k, batch * m * n))
 
 
-# Shapes for the pipelined full-tile kernel (split flow, 256 x 128 tiles):
-# one, two, three and five k chunks (every path of its two-stage loop),
-# several tiles and items, padded leading dimensions.
-BIG_SHAPES = [  # batch, m, n, k, pad
-    (1, 256, 128, 32, 0),
-    (2, 256, 256, 64, 0),
-    (1, 512, 384, 96, 0),
-    (3, 256, 128, 160, 4),
-    (1, 768, 256, 320, 8),
-]
+# Shapes for the pipelined full-tile kernels (split flow): per tile, one,
+# two, three and five k chunks (every path of the two-stage loop), several
+# tiles and items, padded leading dimensions.
+BIG_SHAPES = {  # tile: [(batch, m, n, k, pad)]
+    2: [(1, 128, 128, 32, 0), (2, 256, 256, 64, 0), (1, 384, 128, 96, 4),
+        (3, 128, 256, 160, 8)],
+    3: [(1, 256, 128, 32, 0), (2, 256, 256, 64, 0), (1, 512, 384, 96, 0),
+        (3, 256, 128, 160, 4), (1, 768, 256, 320, 8)],
+    4: [(1, 128, 256, 32, 0), (2, 256, 512, 64, 0), (1, 384, 256, 96, 4),
+        (2, 128, 256, 160, 8)],
+}
+BIG_CASES = [(t, sh) for t, shapes in BIG_SHAPES.items() for sh in shapes]
 
 
-@pytest.mark.parametrize("shape", BIG_SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_full_tile_kernel_shapes(shape):
+@pytest.mark.parametrize("tile,shape", BIG_CASES,
+                         ids=lambda v: str(v) if isinstance(v, int) else "x".join(map(str, v)))
+def test_full_tile_kernel_shapes(tile, shape):
     batch, m, n, k, pad = shape
     dev = device()
-    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128)
-    print(f"case full-tile shape={shape}", flush=True)
+    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, tile)
+    print(f"case full-tile tile={tile} shape={shape}", flush=True)
     A, B = synth.gemm_inputs(batch, m, n, k, seed=51 + m + n + k)
     Ab = torch.zeros((batch, m, k + pad), device=dev)
     Bb = torch.zeros((batch, k, n + pad), device=dev)
@@ -145,14 +148,15 @@ def test_full_tile_kernel_shapes(shape):
     assert kern == "bgemm_big_kernel"
     pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=policy)
     ref = oracle.gemm(A.numpy(), B.numpy())
-    gate(to_np(Cd), ref, k, f"full-tile {shape}")
+    gate(to_np(Cd), ref, k, f"full-tile {tile} {shape}")
 
 
-def test_full_tile_kernel_integer_exact():
+@pytest.mark.parametrize("tile", [2, 3, 4])
+def test_full_tile_kernel_integer_exact(tile):
     g = synth.rng(9)
     A = synth.integer_matrix((2, 256, 96), g, -8, 8)
     B = synth.integer_matrix((2, 96, 256), g, -8, 8)
-    C = _run(A, B, pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    C = _run(A, B, pkg.Policy(pkg.FLOW_SPLIT, 1, tile))
     ref = np.einsum("bik,bkj->bij", A.numpy().astype(np.int64), B.numpy().astype(np.int64))
     assert np.array_equal(C, ref.astype(np.float32))
 
