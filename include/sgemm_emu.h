@@ -151,11 +151,11 @@ int sgemm_emu_batched_ex(int m, int n, int k,
  * nothing is enqueued.  Same validation and errors as sgemm_emu_batched_ex,
  * plus SGEMM_EMU_ERR_NULL for a NULL out; for an empty problem (nothing
  * would run) out receives the policy unresolved.
- * The split flow with error correction and tile 128x128, 256x128 or
- * 128x256 runs a pipelined full-tile kernel when m and n are multiples of
- * the tile, k is a positive multiple of 32 and A and B rows are 16-byte
- * aligned; otherwise the general LDS kernel (128x256 has none:
- * SGEMM_EMU_ERR_POLICY). */
+ * With error correction, the split flow with tile 128x128, 256x128 or
+ * 128x256, and the direct and staged flows with tile 128x128, run a
+ * pipelined full-tile kernel when m and n are multiples of the tile, k is a
+ * positive multiple of 32 and A and B rows are 16-byte aligned; otherwise
+ * the general LDS kernel (128x256 has none: SGEMM_EMU_ERR_POLICY). */
 int sgemm_emu_resolve_policy(int m, int n, int k,
                              const float* A, int lda,
                              const float* B, int ldb,

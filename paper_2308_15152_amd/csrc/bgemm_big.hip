@@ -28,6 +28,20 @@
 // chunk indices past the end are clamped to the last chunk -- so the waits
 // before each use are for that stage's loads only.
 //
+// Flows (where the split happens, the policy of Sec. 4.4 / Fig. 6):
+//   SPLIT  (production) as above: split once per workgroup at staging.
+//   DIRECT LDS holds the FP32 chunk ([row][8 pieces of 4 floats], 128-byte
+//          rows, piece p of row r at p ^ ((r ^ (r >> 3)) & 7), measured
+//          conflict-free for these patterns); every wave reads FP32 operand
+//          values and splits them itself -- the paper's extension-library
+//          flow, fragments built from FP32 shared memory.
+//   STAGED LDS holds the FP32 chunk; every wave converts its own rows and
+//          columns to hi/lo, writes them to a private LDS area and reloads
+//          them as fragments -- the flow a load-only fragment API forces
+//          (three LDS passes per element, twice the footprint).
+// The three have the same tiles, loads and pipeline, so they differ only in
+// LDS traffic and footprint and in where the split's VALU work is done.
+//
 // Only full tiles (m and n multiples of the tile, k of 32) with 16-byte
 // aligned rows; other shapes take the general LDS kernel or the
 // register-direct flow.
@@ -48,10 +62,15 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Tile configuration: BM x BN workgroup tile, WAVES_M x WAVES_N waves of
 // WM x WN (made of 32 x 32 blocks), W waves per SIMD.
-template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int W_, int VALU_PER_MFMA_ = 0>
+enum { BIG_SPLIT = SGEMM_EMU_FLOW_SPLIT, BIG_DIRECT = SGEMM_EMU_FLOW_DIRECT,
+       BIG_STAGED = SGEMM_EMU_FLOW_STAGED };
+
+template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int W_, int VALU_PER_MFMA_ = 0,
+          int FLOW_ = BIG_SPLIT>
 struct BigCfg {
     static constexpr int BM = BM_, BN = BN_, BK = 32;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, W = W_;
+    static constexpr int FLOW = FLOW_;
     // 0: compiler's own schedule; else the MFMAs of a chunk are interleaved
     // with this many VALU instructions each (the split of the next chunk)
     static constexpr int VALU_PER_MFMA = VALU_PER_MFMA_;
@@ -61,8 +80,12 @@ struct BigCfg {
     static constexpr int ROW_BYTES = 2 * BK;  // one row of a binary16 plane
     static constexpr int A_PLANE = BM * ROW_BYTES;
     static constexpr int B_PLANE = BN * ROW_BYTES;
+    // a stage holds the chunk: hi and lo planes (split flow) or the FP32
+    // rows (direct, staged): the same bytes
     static constexpr int STAGE_BYTES = 2 * A_PLANE + 2 * B_PLANE;
-    static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+    // staged flow: each wave's private hi and lo planes of its WM + WN rows
+    static constexpr int WAVE_BYTES = FLOW == BIG_STAGED ? 2 * (WM + WN) * ROW_BYTES : 0;
+    static constexpr int LDS_BYTES = 2 * STAGE_BYTES + (NT / 64) * WAVE_BYTES;
     // staging units: 8 consecutive k of one A row or one B column
     static constexpr int A_UNITS = BM * (BK / 8) / NT;
     static constexpr int B_UNITS = BN * (BK / 8) / NT;
@@ -89,6 +112,12 @@ __device__ inline int piece(int r, int q) {
     return r * 64 + 16 * (q ^ ((r ^ (r >> 2)) & 3));
 }
 
+// Byte offset of piece p (4 floats) of row r in FP32 rows of 128 bytes.
+// Pieces 2q and 2q + 1 sit at offsets that differ only in bit 4.
+__device__ inline int piece32(int r, int p) {
+    return r * 128 + 16 * (p ^ ((r ^ (r >> 3)) & 7));
+}
+
 // Registers of one staged chunk.
 template <class CF>
 struct Stage {
@@ -102,8 +131,8 @@ struct StageMap {
     const float* a[CF::A_UNITS];  // A[m0 + row][8 q]
     const float* b[CF::B_UNITS];  // B[8 kg][n0 + n]
     int64_t ldb;
-    int a_lds[CF::A_UNITS];       // piece(row, q)
-    int b_lds[CF::B_UNITS];       // piece(n, kg)
+    int a_lds[CF::A_UNITS];       // piece(row, q), or piece32(row, 2q) for FP32 stages
+    int b_lds[CF::B_UNITS];       // piece(n, kg), or piece32(n, 2kg)
 };
 
 template <class CF>
@@ -121,10 +150,28 @@ __device__ inline void load_stage(Stage<CF>& st, const StageMap<CF>& sm, int k0)
     }
 }
 
-// Split the staged chunk and write its hi and lo pieces to LDS stage `buf`.
+// Write the staged chunk to LDS stage `buf`: split into hi and lo pieces
+// (split flow) or as FP32 (direct and staged flows).
 template <class CF>
 __device__ inline void store_stage(const Stage<CF>& st, const StageMap<CF>& sm,
                                    unsigned char* buf) {
+    if constexpr (CF::FLOW != BIG_SPLIT) {
+        unsigned char* a32 = buf;
+        unsigned char* b32 = buf + 2 * CF::A_PLANE;
+#pragma unroll
+        for (int u = 0; u < CF::A_UNITS; ++u) {
+            *reinterpret_cast<f32x4*>(a32 + sm.a_lds[u]) = st.a[u][0];
+            *reinterpret_cast<f32x4*>(a32 + (sm.a_lds[u] ^ 16)) = st.a[u][1];
+        }
+#pragma unroll
+        for (int u = 0; u < CF::B_UNITS; ++u) {
+            const f32x4 v0 = {st.b[u][0], st.b[u][1], st.b[u][2], st.b[u][3]};
+            const f32x4 v1 = {st.b[u][4], st.b[u][5], st.b[u][6], st.b[u][7]};
+            *reinterpret_cast<f32x4*>(b32 + sm.b_lds[u]) = v0;
+            *reinterpret_cast<f32x4*>(b32 + (sm.b_lds[u] ^ 16)) = v1;
+        }
+        return;
+    }
     unsigned char* a_hi = buf;
     unsigned char* a_lo = buf + CF::A_PLANE;
     unsigned char* b_hi = buf + 2 * CF::A_PLANE;
@@ -147,30 +194,99 @@ __device__ inline void store_stage(const Stage<CF>& st, const StageMap<CF>& sm,
     }
 }
 
-// Both 16-wide k steps of one chunk from LDS stage `buf`.
+// Read 8 FP32 values (pieces 2q, 2q + 1 of row r) and split them.
+__device__ inline void read_split32(const unsigned char* plane, int r, int q, half8_t& hi,
+                                    half8_t& lo) {
+    const int o = piece32(r, 2 * q);
+    const f32x4 v0 = *reinterpret_cast<const f32x4*>(plane + o);
+    const f32x4 v1 = *reinterpret_cast<const f32x4*>(plane + (o ^ 16));
+    const float x[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+    mfmae::tcec::split8(x, hi, lo);
+}
+
+// Staged flow: the wave converts its WM rows of A and WN columns of B of the
+// FP32 stage `buf` to hi/lo pieces in its private planes `priv` (rows
+// 0..WM-1 for A, WM..WM+WN-1 for B).
+template <class CF>
+__device__ inline void stage_private(const unsigned char* buf, unsigned char* priv, int wrow,
+                                     int wcol, int l) {
+    const unsigned char* a32 = buf;
+    const unsigned char* b32 = buf + 2 * CF::A_PLANE;
+    unsigned char* p_hi = priv;
+    unsigned char* p_lo = priv + (CF::WM + CF::WN) * CF::ROW_BYTES;
+#pragma unroll
+    for (int i = 0; i < (CF::WM + CF::WN) * 4 / 64; ++i) {
+        const int u = i * 64 + l;
+        const int r = u >> 2, q = u & 3;
+        half8_t hi, lo;
+        if (r < CF::WM) read_split32(a32, wrow + r, q, hi, lo);
+        else read_split32(b32, wcol + r - CF::WM, q, hi, lo);
+        *reinterpret_cast<half8_t*>(p_hi + piece(r, q)) = hi;
+        *reinterpret_cast<half8_t*>(p_lo + piece(r, q)) = lo;
+    }
+    // the fragments read below were written by other lanes of this wave
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+}
+
+// Both 16-wide k steps of one chunk from LDS stage `buf` (and, for the
+// staged flow, the wave's private planes `priv`).
 template <class CF>
 __device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
                                      f32x16_t (&cor)[CF::TM][CF::TN], const unsigned char* buf,
-                                     int wrow, int wcol, int g, int j) {
+                                     unsigned char* priv, int wrow, int wcol, int g, int j) {
     const unsigned char* a_hi = buf;
     const unsigned char* a_lo = buf + CF::A_PLANE;
     const unsigned char* b_hi = buf + 2 * CF::A_PLANE;
     const unsigned char* b_lo = b_hi + CF::B_PLANE;
+    int arow = wrow, brow = wcol;
+    if constexpr (CF::FLOW == BIG_STAGED) {
+        stage_private<CF>(buf, priv, wrow, wcol, threadIdx.x & 63);
+        a_hi = priv;
+        a_lo = priv + (CF::WM + CF::WN) * CF::ROW_BYTES;
+        b_hi = a_hi;
+        b_lo = a_lo;
+        arow = 0;
+        brow = CF::WM;
+    }
 #pragma unroll
     for (int s = 0; s < CF::BK / 16; ++s) {
         const int q = 2 * s + g;  // k = 16 s + 8 g + (0..7), the same for A and B
         half8_t ahi[CF::TM], alo[CF::TM], bhi[CF::TN], blo[CF::TN];
+        if constexpr (CF::FLOW == BIG_DIRECT) {
+            // one B block at a time, to keep the split's temporaries few
+            const unsigned char* a32 = buf;
+            const unsigned char* b32 = buf + 2 * CF::A_PLANE;
 #pragma unroll
-        for (int tm = 0; tm < CF::TM; ++tm) {
-            const int o = piece(wrow + 32 * tm + j, q);
-            ahi[tm] = *reinterpret_cast<const half8_t*>(a_hi + o);
-            alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
-        }
+            for (int tm = 0; tm < CF::TM; ++tm)
+                read_split32(a32, wrow + 32 * tm + j, q, ahi[tm], alo[tm]);
 #pragma unroll
-        for (int tn = 0; tn < CF::TN; ++tn) {
-            const int o = piece(wcol + 32 * tn + j, q);
-            bhi[tn] = *reinterpret_cast<const half8_t*>(b_hi + o);
-            blo[tn] = *reinterpret_cast<const half8_t*>(b_lo + o);
+            for (int tn = 0; tn < CF::TN; ++tn) {
+                half8_t bh, bl;
+                read_split32(b32, wcol + 32 * tn + j, q, bh, bl);
+#pragma unroll
+                for (int tm = 0; tm < CF::TM; ++tm) {
+                    acc[tm][tn] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[tm], bh, acc[tm][tn], 0, 0, 0);
+                    cor[tm][tn] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_f16(alo[tm], bh, cor[tm][tn], 0, 0, 0);
+                    cor[tm][tn] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[tm], bl, cor[tm][tn], 0, 0, 0);
+                }
+            }
+            continue;
+        } else {
+#pragma unroll
+            for (int tm = 0; tm < CF::TM; ++tm) {
+                const int o = piece(arow + 32 * tm + j, q);
+                ahi[tm] = *reinterpret_cast<const half8_t*>(a_hi + o);
+                alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
+            }
+#pragma unroll
+            for (int tn = 0; tn < CF::TN; ++tn) {
+                const int o = piece(brow + 32 * tn + j, q);
+                bhi[tn] = *reinterpret_cast<const half8_t*>(b_hi + o);
+                blo[tn] = *reinterpret_cast<const half8_t*>(b_lo + o);
+            }
         }
 #pragma unroll
         for (int tm = 0; tm < CF::TM; ++tm)
@@ -246,14 +362,14 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
         const int unit = u * CF::NT + tid;
         const int row = unit >> 2, q = unit & 3;
         sm.a[u] = Ab + (int64_t)(m0 + row) * p.lda + 8 * q;
-        sm.a_lds[u] = piece(row, q);
+        sm.a_lds[u] = CF::FLOW == BIG_SPLIT ? piece(row, q) : piece32(row, 2 * q);
     }
 #pragma unroll
     for (int u = 0; u < CF::B_UNITS; ++u) {
         const int unit = u * CF::NT + tid;
         const int n = unit % CF::BN, kg = unit / CF::BN;
         sm.b[u] = Bb + (int64_t)(8 * kg) * p.ldb + n0 + n;
-        sm.b_lds[u] = piece(n, kg);
+        sm.b_lds[u] = CF::FLOW == BIG_SPLIT ? piece(n, kg) : piece32(n, 2 * kg);
     }
     sm.ldb = p.ldb;
 
@@ -278,6 +394,7 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
     const int last = nk - 1;
     unsigned char* buf0 = smem;
     unsigned char* buf1 = smem + CF::STAGE_BYTES;
+    unsigned char* priv = smem + 2 * CF::STAGE_BYTES + wave * CF::WAVE_BYTES;
     Stage<CF> r0, r1;
     load_stage<CF>(r0, sm, 0);
     load_stage<CF>(r1, sm, CF::BK * min(1, last));
@@ -289,18 +406,18 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
     // while the same wave splits chunk c + 1 on the VALU.
     int c = 0;
     for (; c + 2 <= nk; c += 2) {
-        compute_stage<CF>(acc, cor, buf0, wrow, wcol, g, j);
+        compute_stage<CF>(acc, cor, buf0, priv, wrow, wcol, g, j);
         store_stage<CF>(r1, sm, buf1);
         load_stage<CF>(r1, sm, CF::BK * min(c + 3, last));
         interleave<CF>();
         lds_barrier();
-        compute_stage<CF>(acc, cor, buf1, wrow, wcol, g, j);
+        compute_stage<CF>(acc, cor, buf1, priv, wrow, wcol, g, j);
         store_stage<CF>(r0, sm, buf0);
         load_stage<CF>(r0, sm, CF::BK * min(c + 4, last));
         interleave<CF>();
         lds_barrier();
     }
-    if (c < nk) compute_stage<CF>(acc, cor, buf0, wrow, wcol, g, j);
+    if (c < nk) compute_stage<CF>(acc, cor, buf0, priv, wrow, wcol, g, j);
 
     // Epilogue: C = main + corr * 2^-11.  Element e of a 32 x 32 block is
     // row 8 (e / 4) + 4 g + e % 4, column j.
@@ -356,6 +473,9 @@ hipError_t launch_big_cfg(const GemmArgs& a, hipStream_t stream) {
 using Big128x256 = BigCfg<128, 256, 2, 4, 2, 4>;
 using Big256x128 = BigCfg<256, 128, 4, 2, 2>;
 using Big128x128 = BigCfg<128, 128, 2, 2, 2>;
+// the paper's two data flows, for measurement, on the 128 x 128 tile
+using Big128x128Direct = BigCfg<128, 128, 2, 2, 2, 0, BIG_DIRECT>;
+using Big128x128Staged = BigCfg<128, 128, 2, 2, 2, 0, BIG_STAGED>;
 
 template <class CF>
 bool fits(const GemmArgs& a) {
@@ -365,7 +485,11 @@ bool fits(const GemmArgs& a) {
 
 }  // namespace
 
-bool big_supported(const GemmArgs& a, int tile) {
+bool big_supported(const GemmArgs& a, int tile, int flow) {
+    if (flow != SGEMM_EMU_FLOW_SPLIT)
+        return tile == SGEMM_EMU_TILE_128x128 &&
+               (flow == SGEMM_EMU_FLOW_DIRECT || flow == SGEMM_EMU_FLOW_STAGED) &&
+               fits<Big128x128>(a);
     switch (tile) {
         case SGEMM_EMU_TILE_128x128: return fits<Big128x128>(a);
         case SGEMM_EMU_TILE_256x128: return fits<Big256x128>(a);
@@ -374,8 +498,10 @@ bool big_supported(const GemmArgs& a, int tile) {
     }
 }
 
-hipError_t launch_gemm_big(const GemmArgs& a, int tile, hipStream_t stream) {
-    if (!big_supported(a, tile)) return hipErrorInvalidValue;
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream) {
+    if (!big_supported(a, tile, flow)) return hipErrorInvalidValue;
+    if (flow == SGEMM_EMU_FLOW_DIRECT) return launch_big_cfg<Big128x128Direct>(a, stream);
+    if (flow == SGEMM_EMU_FLOW_STAGED) return launch_big_cfg<Big128x128Staged>(a, stream);
     switch (tile) {
         case SGEMM_EMU_TILE_128x128: return launch_big_cfg<Big128x128>(a, stream);
         case SGEMM_EMU_TILE_256x128: return launch_big_cfg<Big256x128>(a, stream);

@@ -117,7 +117,7 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
                                   SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
             for (int t : order)
                 if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&
-                    sgemm_emu::big_supported(a, t))
+                    sgemm_emu::big_supported(a, t, SGEMM_EMU_FLOW_SPLIT))
                     big_tile = t;
         }
         if (big_tile != SGEMM_EMU_TILE_AUTO) {
@@ -135,7 +135,7 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
         kern = K_REG;
-    } else if (flow == SGEMM_EMU_FLOW_SPLIT && ec == 1 && sgemm_emu::big_supported(a, tile)) {
+    } else if (ec == 1 && sgemm_emu::big_supported(a, tile, flow)) {
         kern = K_BIG;  // full tiles: the pipelined kernel
     } else if (tile != SGEMM_EMU_TILE_128x256 && sgemm_emu::gemm_variant_exists(tile, flow)) {
         kern = K_LDS;
@@ -155,7 +155,7 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
     hipError_t e;
     switch (kern) {
         case K_REG: e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream); break;
-        case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, stream); break;
+        case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, flow, stream); break;
         default: e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream); break;
     }
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);

@@ -31,10 +31,11 @@ bool gemm_variant_exists(int tile, int flow);
 bool reg_flow_supported(const GemmArgs& a, int tile);
 hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t stream);
 
-// Pipelined full-tile kernels (split flow; tiles 128x128, 256x128,
-// 128x256): true if the shape and alignment allow the tile.
-bool big_supported(const GemmArgs& a, int tile);
-hipError_t launch_gemm_big(const GemmArgs& a, int tile, hipStream_t stream);
+// Pipelined full-tile kernels (split flow: tiles 128x128, 256x128,
+// 128x256; direct and staged flows: tile 128x128): true if the shape and
+// alignment allow the tile.
+bool big_supported(const GemmArgs& a, int tile, int flow);
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream);
 
 struct HouseholderArgs {
     int ncols;

@@ -151,6 +151,11 @@ def test_resolve_policy():
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
     assert _resolve.kernel == "bgemm_emu_kernel"
+    # the paper's flows on full 128 x 128 tiles run in the full-tile kernel
+    for flow in (pkg.FLOW_DIRECT, pkg.FLOW_STAGED):
+        assert _resolve(8192, 8192, 8192, policy=pkg.Policy(flow, 1, pkg.TILE_128x128)) == (
+            0, (flow, 1, pkg.TILE_128x128))
+        assert _resolve.kernel == "bgemm_big_kernel"
     pol = pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_64x64)
     assert _resolve(128, 128, 128, policy=pol) == (0, (pkg.FLOW_DIRECT, 0, pkg.TILE_64x64))
     # the 128x256 tile exists only for full tiles of the split flow

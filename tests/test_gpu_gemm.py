@@ -127,16 +127,20 @@ BIG_SHAPES = {  # tile: [(batch, m, n, k, pad)]
     4: [(1, 128, 256, 32, 0), (2, 256, 512, 64, 0), (1, 384, 256, 96, 4),
         (2, 128, 256, 160, 8)],
 }
-BIG_CASES = [(t, sh) for t, shapes in BIG_SHAPES.items() for sh in shapes]
+# the 128 x 128 tile also runs the paper's direct and staged data flows
+BIG_CASES = [(f, t, sh) for t, shapes in BIG_SHAPES.items()
+             for f in ([pkg.FLOW_SPLIT, pkg.FLOW_DIRECT, pkg.FLOW_STAGED] if t == 2
+                       else [pkg.FLOW_SPLIT])
+             for sh in shapes]
 
 
-@pytest.mark.parametrize("tile,shape", BIG_CASES,
+@pytest.mark.parametrize("flow,tile,shape", BIG_CASES,
                          ids=lambda v: str(v) if isinstance(v, int) else "x".join(map(str, v)))
-def test_full_tile_kernel_shapes(tile, shape):
+def test_full_tile_kernel_shapes(flow, tile, shape):
     batch, m, n, k, pad = shape
     dev = device()
-    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, tile)
-    print(f"case full-tile tile={tile} shape={shape}", flush=True)
+    policy = pkg.Policy(flow, 1, tile)
+    print(f"case full-tile flow={flow} tile={tile} shape={shape}", flush=True)
     A, B = synth.gemm_inputs(batch, m, n, k, seed=51 + m + n + k)
     Ab = torch.zeros((batch, m, k + pad), device=dev)
     Bb = torch.zeros((batch, k, n + pad), device=dev)
