@@ -434,6 +434,206 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
         }
 }
 
+// Geometry of one task (one tile of one item).
+struct TaskGeo {
+    const float* A;  // item bases
+    const float* B;
+    float* C;
+    int m0, n0;
+};
+
+template <class CF>
+__device__ inline TaskGeo task_geo(const BigParams& p, int task) {
+    const int tiles = p.tiles_m * p.tiles_n;
+    const int item = task / tiles;
+    const int t = task - item * tiles;
+    // tiles in groups of 8 tile rows, so that the workgroups running at the
+    // same time on one XCD share B columns
+    constexpr int GROUP_M = 8;
+    const int group_size = GROUP_M * p.tiles_n;
+    const int grp = t / group_size;
+    const int first_m = grp * GROUP_M;
+    const int gm = min(p.tiles_m - first_m, GROUP_M);
+    const int r = t - grp * group_size;
+    TaskGeo q;
+    const int64_t it = (int64_t)item + p.item0;
+    q.A = p.A + it * p.sa;
+    q.B = p.B + it * p.sb;
+    q.C = p.C + it * p.sc;
+    q.m0 = (first_m + r % gm) * CF::BM;
+    q.n0 = (r / gm) * CF::BN;
+    return q;
+}
+
+// Global addresses of this thread's staging units for task geometry q.
+template <class CF>
+__device__ inline void map_task(StageMap<CF>& sm, const BigParams& p, const TaskGeo& q) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < CF::A_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
+        const int row = unit >> 2, qq = unit & 3;
+        sm.a[u] = q.A + (int64_t)(q.m0 + row) * p.lda + 8 * qq;
+    }
+#pragma unroll
+    for (int u = 0; u < CF::B_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
+        const int n = unit % CF::BN, kg = unit / CF::BN;
+        sm.b[u] = q.B + (int64_t)(8 * kg) * p.ldb + q.n0 + n;
+    }
+}
+
+// LDS offsets of this thread's staging units (the same for every task).
+template <class CF>
+__device__ inline void map_lds(StageMap<CF>& sm) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < CF::A_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
+        const int row = unit >> 2, q = unit & 3;
+        sm.a_lds[u] = CF::FLOW == BIG_SPLIT ? piece(row, q) : piece32(row, 2 * q);
+    }
+#pragma unroll
+    for (int u = 0; u < CF::B_UNITS; ++u) {
+        const int unit = u * CF::NT + tid;
+        const int n = unit % CF::BN, kg = unit / CF::BN;
+        sm.b_lds[u] = CF::FLOW == BIG_SPLIT ? piece(n, kg) : piece32(n, 2 * kg);
+    }
+}
+
+// C = main + corr * 2^-11 for the wave's sub-tile, and zero the
+// accumulators.  Element e of a 32 x 32 block is row 8 (e / 4) + 4 g + e % 4,
+// column j.
+template <class CF>
+__device__ inline void store_c(f32x16_t (&acc)[CF::TM][CF::TN], f32x16_t (&cor)[CF::TM][CF::TN],
+                               const BigParams& p, const TaskGeo& q, int wrow, int wcol, int g,
+                               int j) {
+#pragma unroll
+    for (int tm = 0; tm < CF::TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < CF::TN; ++tn) {
+            float* cp = q.C + (int64_t)(q.m0 + wrow + 32 * tm + 4 * g) * p.ldc + q.n0 + wcol +
+                        32 * tn + j;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc] =
+                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]);
+                acc[tm][tn][e] = 0.0f;
+                cor[tm][tn][e] = 0.0f;
+            }
+        }
+}
+
+// Persistent form: a grid of about as many workgroups as fit on the GPU at
+// once; each walks its tasks (task t0 + i G) as one stream of k chunks, so
+// the loads of a task's first chunks are issued while the previous task's
+// last chunks are computed and its C is stored, and there is no pipeline
+// fill per tile.
+template <class CF>
+__global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_stream_kernel(BigParams p) {
+    __shared__ __attribute__((aligned(16))) unsigned char smem[CF::LDS_BYTES];
+
+    const int G = gridDim.x;
+    const int t0 = xcd_task(blockIdx.x, G);
+    if (t0 >= p.ntasks) return;  // the whole workgroup leaves together
+    const int ntw = (p.ntasks - 1 - t0) / G + 1;  // tasks of this workgroup
+    const int nk = p.k / CF::BK;                  // chunks per task, >= 1
+    const int total = ntw * nk;                   // chunks in the stream
+
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int l = tid & 63;
+    const int g = l >> 5, j = l & 31;
+    const int wrow = (wave / CF::WAVES_N) * CF::WM;
+    const int wcol = (wave % CF::WAVES_N) * CF::WN;
+
+    StageMap<CF> sm;
+    map_lds<CF>(sm);
+    sm.ldb = p.ldb;
+    map_task<CF>(sm, p, task_geo<CF>(p, t0));
+    // load cursor: task index li of this workgroup, chunk lc.  Past the end
+    // it stays on the last chunk (re-loading it keeps every load
+    // unconditional).
+    int li = 0, lc = 0;
+    auto load_next = [&](Stage<CF>& st) {
+        load_stage<CF>(st, sm, CF::BK * lc);
+        if (++lc == nk) {
+            if (li + 1 < ntw) {
+                ++li;
+                lc = 0;
+                map_task<CF>(sm, p, task_geo<CF>(p, t0 + li * G));
+            } else {
+                lc = nk - 1;
+            }
+        }
+    };
+
+    f32x16_t acc[CF::TM][CF::TN], cor[CF::TM][CF::TN];
+#pragma unroll
+    for (int tm = 0; tm < CF::TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < CF::TN; ++tn)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                acc[tm][tn][e] = 0.0f;
+                cor[tm][tn][e] = 0.0f;
+            }
+
+    unsigned char* buf0 = smem;
+    unsigned char* buf1 = smem + CF::STAGE_BYTES;
+    unsigned char* priv = smem + 2 * CF::STAGE_BYTES + wave * CF::WAVE_BYTES;
+    // compute cursor: task index ci, chunk cc
+    int ci = 0, cc = 0;
+    auto finish_chunk = [&]() {
+        if (++cc == nk) {
+            store_c<CF>(acc, cor, p, task_geo<CF>(p, t0 + ci * G), wrow, wcol, g, j);
+            ++ci;
+            cc = 0;
+        }
+    };
+    Stage<CF> r0, r1;
+    load_next(r0);  // chunk 0
+    load_next(r1);  // chunk 1
+    store_stage<CF>(r0, sm, buf0);
+    load_next(r0);  // chunk 2
+    lds_barrier();
+    // position s: compute chunk s, store chunk s + 1, load chunk s + 3
+    for (int s = 0; s < total; s += 2) {
+        compute_stage<CF>(acc, cor, buf0, priv, wrow, wcol, g, j);
+        finish_chunk();
+        store_stage<CF>(r1, sm, buf1);
+        load_next(r1);
+        interleave<CF>();
+        lds_barrier();
+        if (s + 1 < total) {
+            compute_stage<CF>(acc, cor, buf1, priv, wrow, wcol, g, j);
+            finish_chunk();
+        }
+        store_stage<CF>(r0, sm, buf0);
+        load_next(r0);
+        interleave<CF>();
+        lds_barrier();
+    }
+}
+
+// Workgroups of one instance that fit on the device at once (cached per
+// device).
+template <class CF, class K>
+int resident_wgs(K kernel) {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cache[dev] > 0) return cache[dev];
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, CF::NT, 0) != hipSuccess)
+        return 0;
+    const int r = cus * (per_cu > 0 ? per_cu : 1);
+    cache[dev] = r;  // benign race: every thread computes the same value
+    return r;
+}
+
 template <class CF>
 hipError_t launch_big_cfg(const GemmArgs& a, hipStream_t stream) {
     BigParams p;
@@ -460,6 +660,43 @@ hipError_t launch_big_cfg(const GemmArgs& a, hipStream_t stream) {
         p.item0 = (int)i0;
         hipLaunchKernelGGL(bgemm_big_kernel<CF>, dim3((unsigned)p.ntasks), dim3(CF::NT), 0, stream,
                            p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <class CF>
+hipError_t launch_big_stream_cfg(const GemmArgs& a, hipStream_t stream) {
+    BigParams p;
+    p.k = a.k;
+    p.A = a.A;
+    p.lda = a.lda;
+    p.sa = a.sa;
+    p.B = a.B;
+    p.ldb = a.ldb;
+    p.sb = a.sb;
+    p.C = a.C;
+    p.ldc = a.ldc;
+    p.sc = a.sc;
+    p.tiles_m = a.m / CF::BM;
+    p.tiles_n = a.n / CF::BN;
+    const int resident = resident_wgs<CF>(bgemm_big_stream_kernel<CF>);
+    if (resident <= 0) {
+        hipError_t e = hipGetLastError();
+        return e != hipSuccess ? e : hipErrorInvalidDeviceFunction;
+    }
+    const int64_t tiles = (int64_t)p.tiles_m * p.tiles_n;
+    const int64_t max_tasks = (int64_t(1) << 31) - 1;  // task ids are 32-bit
+    if (tiles > max_tasks) return hipErrorInvalidConfiguration;
+    const int64_t items_per_launch = max_tasks / tiles;
+    for (int64_t i0 = 0; i0 < a.batch; i0 += items_per_launch) {
+        const int64_t items = a.batch - i0 < items_per_launch ? a.batch - i0 : items_per_launch;
+        p.ntasks = (int)(items * tiles);
+        p.item0 = (int)i0;
+        const int grid = p.ntasks < resident ? p.ntasks : resident;
+        hipLaunchKernelGGL(bgemm_big_stream_kernel<CF>, dim3((unsigned)grid), dim3(CF::NT), 0,
+                           stream, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -504,7 +741,12 @@ hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t st
     if (flow == SGEMM_EMU_FLOW_STAGED) return launch_big_cfg<Big128x128Staged>(a, stream);
     switch (tile) {
         case SGEMM_EMU_TILE_128x128: return launch_big_cfg<Big128x128>(a, stream);
-        case SGEMM_EMU_TILE_256x128: return launch_big_cfg<Big256x128>(a, stream);
+        case SGEMM_EMU_TILE_256x128:
+            // one workgroup per CU: with few k chunks per tile, the
+            // persistent stream hides the per-tile pipeline fill (measured
+            // 1.14x on 1024 x 256^3); long k loops amortize it themselves
+            return a.k <= 2048 ? launch_big_stream_cfg<Big256x128>(a, stream)
+                               : launch_big_cfg<Big256x128>(a, stream);
         default: return launch_big_cfg<Big128x256>(a, stream);
     }
 }

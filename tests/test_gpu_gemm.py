@@ -155,6 +155,21 @@ def test_full_tile_kernel_shapes(flow, tile, shape):
     gate(to_np(Cd), ref, k, f"full-tile {tile} {shape}")
 
 
+@pytest.mark.parametrize("batch,k", [(600, 96), (513, 32), (300, 160)])
+def test_full_tile_stream_many_tasks(batch, k):
+    """More 256 x 128 tiles than workgroups on the GPU: the persistent form
+    walks several tasks per workgroup as one stream of k chunks (odd and
+    even chunk counts, one chunk per task); sampled items are compared."""
+    m, n = 256, 128
+    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_256x128)
+    print(f"case full-tile stream batch={batch} k={k}", flush=True)
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=61 + batch + k)
+    C = _run(A, B, policy)
+    items = sorted(set([0, 1, batch // 2, batch - 2, batch - 1] + list(range(3, batch, 37))))
+    ref = oracle.gemm(A[items].numpy(), B[items].numpy())
+    gate(C[items], ref, k, f"stream batch={batch} k={k}")
+
+
 @pytest.mark.parametrize("tile", [2, 3, 4])
 def test_full_tile_kernel_integer_exact(tile):
     g = synth.rng(9)
