@@ -82,9 +82,9 @@ int sgemm_emu_batched(int m, int n, int k,
  * flow:
  *   SGEMM_EMU_FLOW_AUTO   library choice: SPLIT on full tiles when a
  *                         full-tile kernel applies (see
- *                         sgemm_emu_resolve_policy): 128x256 for products
- *                         of at least 2048 x 2048, else 256x128, else
- *                         128x128; otherwise REG for products up to
+ *                         sgemm_emu_resolve_policy): 128x256 when k >= 1024
+ *                         and batch * m * n >= 2048 * 2048, else 256x128,
+ *                         else 128x128; otherwise REG for products up to
  *                         1024 x 1024 whose operands allow its vector loads;
  *                         otherwise SPLIT.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the

@@ -112,8 +112,10 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
         const int reg_tile = (m <= 64 && n <= 64) ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
         int big_tile = SGEMM_EMU_TILE_AUTO;
         if (ec == 1) {
-            const int order[3] = {(int64_t)m * n >= 2048 * 2048 ? SGEMM_EMU_TILE_128x256
-                                                                 : SGEMM_EMU_TILE_256x128,
+            // 128x256 pays off for long k loops over much output (measured on
+            // 8192^3 and on 256 x 1024 x 1024 x k for k >= 1024)
+            const bool wide = k >= 1024 && (int64_t)m * n * batch >= (int64_t)2048 * 2048;
+            const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
                                   SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
             for (int t : order)
                 if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&

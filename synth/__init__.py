@@ -18,6 +18,8 @@ Workloads (row-major, contiguous, FP32):
 * ``gemm_8192``  batch 1,      8192 x 8192 x 8192, entries uniform(-1, 1), seed 4
 * ``householder_64``  batch 262144, u in R^64 standard normal then divided by
   its FP32 2-norm, B 64 x 64 uniform(-1, 1),                               seed 5
+* ``paper_k<K>``  batch 256, 1024 x 1024 x K for K in PAPER_SWEEP_K,
+  entries uniform(-1, 1),                                                  seed 6
 
 uniform(-1, 1) is drawn as ``2 * torch.rand - 1`` in FP32, which is exact and
 lies on a 2^-23 grid.
@@ -66,6 +68,14 @@ WORKLOADS = {
     "householder_64": Workload("householder_64", "householder", 262144, 64, 64, 64,
                                "householder", 5),
 }
+
+# The batched SGEMM experiment of Sec. 4.4.2: 256 products of
+# (1024 x k) . (k x 1024), swept over k (the k values are only in the
+# paper's missing figure; these span its range of shapes).
+PAPER_SWEEP_K = (128, 256, 512, 1024, 2048, 4096)
+for _k in PAPER_SWEEP_K:
+    WORKLOADS[f"paper_k{_k}"] = Workload(f"paper_k{_k}", "gemm", 256, 1024, 1024, _k,
+                                         "uniform", 6)
 
 
 def _gen(seed: int) -> torch.Generator:

@@ -343,3 +343,21 @@ def test_workload_gemm_8192_sampled():
     ref = oracle.dots(An[rows], np.ascontiguousarray(Bn[:, cols].T))
     e = gate(C[rows, cols], ref, w.k, "gemm_8192")
     print(f"gemm_8192: err {e[0]:.3e} fp32 {e[1]:.3e}")
+
+
+def test_workload_paper_sweep_k256_sampled():
+    """The batched experiment of Sec. 4.4.2 at k = 256 (256 products of
+    1024 x 256 . 256 x 1024), in the configuration the sweep times, checked
+    on sampled elements of sampled items."""
+    w = synth.WORKLOADS["paper_k256"]
+    print("case workload=paper_k256", flush=True)
+    A, B = synth.workload_inputs(w)
+    C = _run(A, B)
+    g = np.random.default_rng(256)
+    items = [0, 97, 255]
+    for it in items:
+        rows = g.integers(0, w.m, 300)
+        cols = g.integers(0, w.n, 300)
+        ref = oracle.dots(A[it].numpy()[rows], np.ascontiguousarray(B[it].numpy()[:, cols].T))
+        gate(C[it][rows, cols], ref, w.k, f"paper_k256 item {it}")
+
