@@ -141,8 +141,11 @@ def test_resolve_policy():
     assert _resolve.kernel == "bgemm_big_kernel"
     # the batched experiment of Sec. 4.4.2: 128x256 from k = 1024 on
     s1m = 1024 * 1024
-    assert _resolve(1024, 1024, 512, 256, (1024 * 512, 512 * 1024, s1m))[1][2] == pkg.TILE_256x128
-    assert _resolve(1024, 1024, 1024, 256, (s1m, s1m, s1m))[1][2] == pkg.TILE_128x256
+    far = dict(A=1 << 40, B=2 << 40, C=3 << 40)  # gigabytes apart: no overlap
+    assert _resolve(1024, 1024, 512, 256, (1024 * 512, 512 * 1024, s1m),
+                    **far) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve(1024, 1024, 1024, 256, (s1m, s1m, s1m),
+                    **far) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
     assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
                                                                  pkg.TILE_64x64))
     assert _resolve.kernel == "bgemm_reg_kernel"
