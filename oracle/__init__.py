@@ -21,6 +21,9 @@ it follows:
   FP64.
 * :func:`householder` -- H = I - 2 u u^T formed explicitly and applied to B
   (Sec. 4.2.1, eq. householder, read as an outer product of u).
+* :func:`givens_matrix`, :func:`givens` -- the rotation G(i, j, theta) of
+  Sec. 4.3.1 (identity except G_ii = G_jj = c, G_ij = -s, G_ji = s) formed
+  explicitly from the FP32 c and s and applied to B.
 * :func:`max_rel_err` -- the "max relative error" of Sec. 4.4.2, normalised
   per element by (|A||B|)_ij, evaluated in FP64.
 """
@@ -68,6 +71,11 @@ def _load():
     lib.oracle_householder.argtypes = [i32, i32, i32, P, P, i64, P, i64, i64,
                                        P, P, P, P, i64, i64]
     lib.oracle_householder.restype = None
+    lib.oracle_givens_matrix.argtypes = [i32, i32, i32, ctypes.c_float, ctypes.c_float, P]
+    lib.oracle_givens_matrix.restype = None
+    lib.oracle_givens.argtypes = [i32, i32, i32, i32, i32, P, P, P, i64, P, i64, i64,
+                                  P, P, P, P, i64, i64]
+    lib.oracle_givens.restype = None
     _lib = lib
     return lib
 
@@ -209,6 +217,44 @@ def householder(u: np.ndarray, B: np.ndarray, items=None,
     _load().oracle_householder(n, ncols, t, _ptr(items), _ptr(u), n, _ptr(B),
                                ncols, n * ncols, _ptr(out["c64"]), _ptr(out["n64"]),
                                _ptr(out["c32"]), _ptr(out["cm"]), ncols, n * ncols)
+    return {key: v for key, v in out.items() if v is not None}
+
+
+# --------------------------------------------------------------------------
+# Givens oracle (Sec. 4.3.1)
+# --------------------------------------------------------------------------
+
+def givens_matrix(n: int, i: int, j: int, c, s) -> np.ndarray:
+    """The n x n rotation G(i, j, theta) with c = cos theta, s = sin theta
+    given as FP32 values: FP32, every entry one of 0, 1, c, s, -s."""
+    assert 0 <= i < n and 0 <= j < n and i != j
+    G = np.empty((n, n), dtype=np.float32)
+    _load().oracle_givens_matrix(n, i, j, float(np.float32(c)), float(np.float32(s)), _ptr(G))
+    return G
+
+
+def givens(i: int, j: int, c: np.ndarray, s: np.ndarray, B: np.ndarray, items=None,
+           want=("c64", "n64", "c32", "cm")):
+    """Oracle quantities for C_b = G(i, j, theta_b) B_b.
+
+    c, s: [batch] FP32; B: [batch, n, ncols].  ``items`` selects which batch
+    items to evaluate (default: all); the outputs are [len(items), n, ncols]."""
+    c = _f32(c).reshape(-1)
+    s = _f32(s).reshape(-1)
+    B = _f32(B)
+    batch, n, ncols = B.shape
+    assert c.shape == (batch,) and s.shape == (batch,)
+    assert 0 <= i < n and 0 <= j < n and i != j
+    items = np.arange(batch, dtype=np.int64) if items is None else \
+        np.ascontiguousarray(items, dtype=np.int64)
+    t = items.shape[0]
+    out = {}
+    for key, dt in (("c64", np.float64), ("n64", np.float64),
+                    ("c32", np.float32), ("cm", np.float64)):
+        out[key] = np.zeros((t, n, ncols), dtype=dt) if key in want else None
+    _load().oracle_givens(n, i, j, ncols, t, _ptr(items), _ptr(c), _ptr(s), 1, _ptr(B),
+                          ncols, n * ncols, _ptr(out["c64"]), _ptr(out["n64"]),
+                          _ptr(out["c32"]), _ptr(out["cm"]), ncols, n * ncols)
     return {key: v for key, v in out.items() if v is not None}
 
 

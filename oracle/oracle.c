@@ -25,6 +25,9 @@
  *     (Sec. 4.4, eq. corr-5).
  *   - oracle_householder: H = I - 2 u u^T built explicitly and applied to
  *     B (Sec. 4.2.1, eq. householder, read as an outer product).
+ *   - oracle_givens: the rotation G(i, j, theta) of Sec. 4.3.1 (identity
+ *     except G_ii = G_jj = c, G_ij = -s, G_ji = s) built explicitly and
+ *     applied to B, with c and s given as FP32 values.
  *
  * Compile with -ffp-contract=off so that only the explicit fmaf/fma calls
  * fuse.
@@ -280,6 +283,85 @@ void oracle_householder(int n, int ncols, int nitems, const int64_t *items,
                         double bh = oracle_f16_to_f32(hb);
                         double al = oracle_f16_to_f32(oracle_f32_to_f16(
                             (h32 - (float)ah) * 2048.0f));
+                        double bl = oracle_f16_to_f32(oracle_f32_to_f16(
+                            (bv - (float)bh) * 2048.0f));
+                        sm += ah * bh + (al * bh + ah * bl) / 2048.0;
+                    }
+                }
+                int64_t o = (int64_t)t * sc + (int64_t)i * ldc + j;
+                if (C64)
+                    C64[o] = s64;
+                if (N64)
+                    N64[o] = nrm;
+                if (C32)
+                    C32[o] = s32;
+                if (CM)
+                    CM[o] = sm;
+            }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Givens rotation: C = G(i, j, theta) B, G formed explicitly (Sec. 4.3.1) */
+/* ---------------------------------------------------------------------- */
+
+/* Entry (r, q) of the n x n rotation in the (i, j) plane: the identity
+ * except G_ii = G_jj = c, G_ij = -s, G_ji = s.  Every entry is one of the
+ * FP32 values 0, 1, c, s, -s, so the FP32 and FP64 matrices are equal. */
+static float givens_entry(int r, int q, int i, int j, float c, float s)
+{
+    if ((r == i && q == i) || (r == j && q == j))
+        return c;
+    if (r == i && q == j)
+        return -s;
+    if (r == j && q == i)
+        return s;
+    return r == q ? 1.0f : 0.0f;
+}
+
+void oracle_givens_matrix(int n, int i, int j, float c, float s, float *G)
+{
+    for (int r = 0; r < n; ++r)
+        for (int q = 0; q < n; ++q)
+            G[(int64_t)r * n + q] = givens_entry(r, q, i, j, c, s);
+}
+
+/* Batched application.  Per item b: c_b = c[b * scs], s_b = s[b * scs],
+ * B_b (n x ncols, ldb, item stride sb); outputs n x ncols with row stride
+ * ldc and item stride sc:
+ *   C64 = G B, N64 = |G| |B|, C32 = fmaf chain of G B (k ascending),
+ *   CM  = method-exact model of the emulated product G * B.
+ * Only items listed in `items` are computed; output slot t receives item
+ * items[t]. */
+void oracle_givens(int n, int gi, int gj, int ncols, int nitems, const int64_t *items,
+                   const float *c, const float *s, int64_t scs,
+                   const float *B, int64_t ldb, int64_t sb,
+                   double *C64, double *N64, float *C32, double *CM,
+                   int64_t ldc, int64_t sc)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int t = 0; t < nitems; ++t) {
+        int64_t b = items[t];
+        float cb = c[b * scs], sbv = s[b * scs];
+        const float *Bb = B + b * sb;
+        for (int i = 0; i < n; ++i) {
+            for (int j = 0; j < ncols; ++j) {
+                double s64 = 0.0, nrm = 0.0, sm = 0.0;
+                float s32 = 0.0f;
+                for (int kk = 0; kk < n; ++kk) {
+                    float g = givens_entry(i, kk, gi, gj, cb, sbv);
+                    float bv = Bb[(int64_t)kk * ldb + j];
+                    s64 += (double)g * (double)bv;
+                    nrm += fabs((double)g) * fabs((double)bv);
+                    s32 = fmaf(g, bv, s32);
+                    if (CM) {
+                        uint16_t ha = oracle_f32_to_f16(g);
+                        uint16_t hb = oracle_f32_to_f16(bv);
+                        double ah = oracle_f16_to_f32(ha);
+                        double bh = oracle_f16_to_f32(hb);
+                        double al = oracle_f16_to_f32(oracle_f32_to_f16(
+                            (g - (float)ah) * 2048.0f));
                         double bl = oracle_f16_to_f32(oracle_f32_to_f16(
                             (bv - (float)bh) * 2048.0f));
                         sm += ah * bh + (al * bh + ah * bl) / 2048.0;

@@ -20,6 +20,9 @@ Workloads (row-major, contiguous, FP32):
   its FP32 2-norm, B 64 x 64 uniform(-1, 1),                               seed 5
 * ``paper_k<K>``  batch 256, 1024 x 1024 x K for K in PAPER_SWEEP_K,
   entries uniform(-1, 1),                                                  seed 6
+* ``givens_64``  batch 262144, rotation plane (i, j) = (5, 37) of n = 64,
+  theta uniform in [0, 2 pi) per item with c, s = cos, sin theta evaluated
+  in FP64 and rounded to FP32, B 64 x 64 uniform(-1, 1),                   seed 7
 
 uniform(-1, 1) is drawn as ``2 * torch.rand - 1`` in FP32, which is exact and
 lies on a 2^-23 grid.
@@ -34,27 +37,31 @@ import torch
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str        # "gemm" or "householder"
+    kind: str        # "gemm", "householder" or "givens"
     batch: int
     m: int
     n: int
     k: int
     dist: str        # "uniform" or "uniform_exp"
     seed: int
+    plane: tuple = (0, 1)   # rotation plane (i, j) of a Givens workload
 
     @property
     def flops(self) -> float:
         """Emulated flops counted as 2 m n k per item (Sec. 4.4.2); for the
-        Householder workload H is formed explicitly, so the same dense count
-        applies with m = k = 64."""
+        Householder and Givens workloads the left matrix is formed
+        explicitly as a fragment, so the same dense count applies with
+        m = k = 64."""
         return 2.0 * self.m * self.n * self.k * self.batch
 
     @property
     def algorithmic_bytes(self) -> int:
-        """Bytes the product must move at least once: read A (or u) and B,
-        write C, all FP32."""
+        """Bytes the product must move at least once: read A (or u, or c
+        and s) and B, write C, all FP32."""
         if self.kind == "householder":
             per = 4 * (self.m + self.k * self.n + self.m * self.n)
+        elif self.kind == "givens":
+            per = 4 * (2 + self.k * self.n + self.m * self.n)
         else:
             per = 4 * (self.m * self.k + self.k * self.n + self.m * self.n)
         return per * self.batch
@@ -76,6 +83,10 @@ PAPER_SWEEP_K = (128, 256, 512, 1024, 2048, 4096)
 for _k in PAPER_SWEEP_K:
     WORKLOADS[f"paper_k{_k}"] = Workload(f"paper_k{_k}", "gemm", 256, 1024, 1024, _k,
                                          "uniform", 6)
+
+
+WORKLOADS["givens_64"] = Workload("givens_64", "givens", 262144, 64, 64, 64, "givens", 7,
+                                  (5, 37))
 
 
 def _gen(seed: int) -> torch.Generator:
@@ -117,6 +128,18 @@ def householder_inputs(batch: int, n: int, ncols: int, seed: int):
     return u, B
 
 
+def givens_inputs(batch: int, n: int, ncols: int, seed: int):
+    """c [batch], s [batch] (theta uniform in [0, 2 pi), cos and sin in FP64
+    rounded to FP32), then B [batch, n, ncols] uniform(-1, 1), drawn in that
+    order."""
+    g = _gen(seed)
+    theta = torch.rand((batch,), generator=g, dtype=torch.float64) * (2.0 * torch.pi)
+    c = torch.cos(theta).to(torch.float32)
+    s = torch.sin(theta).to(torch.float32)
+    B = uniform((batch, n, ncols), g)
+    return c, s, B
+
+
 def workload_inputs(w: Workload, batch: int | None = None):
     """Inputs of a named workload; ``batch`` may shrink the batch (the first
     items are then a prefix of what a smaller draw would give only for the
@@ -124,6 +147,8 @@ def workload_inputs(w: Workload, batch: int | None = None):
     b = w.batch if batch is None else batch
     if w.kind == "householder":
         return householder_inputs(b, w.m, w.n, w.seed)
+    if w.kind == "givens":
+        return givens_inputs(b, w.m, w.n, w.seed)
     return gemm_inputs(b, w.m, w.n, w.k, w.seed, w.dist)
 
 
