@@ -57,7 +57,9 @@ KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are ad
     "bgemm_reg_kernel": "bgemm_reg.hip",
     "bgemm_big_kernel": "bgemm_big.hip",
     "bgemm_emu_kernel": "bgemm.hip",
-    "householder64_kernel": "householder.hip",
+    "householder64_kernel": "rulebuilt.hip",
+    "givens64_kernel": "rulebuilt.hip",
+    "givens64_lds_kernel": "rulebuilt.hip",
 }
 
 
@@ -93,6 +95,10 @@ def measured_traffic(workload: str, kernel: str):
 
 
 
+GIVENS_MODES = {"auto": pkg.GIVENS_AUTO, "map": pkg.GIVENS_MAP,
+                "embedded": pkg.GIVENS_EMBEDDED, "lds": pkg.GIVENS_LDS}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,6 +108,10 @@ def parse():
     ap.add_argument("--flow", type=int, default=pkg.FLOW_AUTO)
     ap.add_argument("--ec", type=int, default=1)
     ap.add_argument("--tile", type=int, default=pkg.TILE_AUTO)
+    ap.add_argument("--givens-mode", default="auto", choices=sorted(GIVENS_MODES),
+                    help="how a Givens workload builds G: map with (i, j) as kernel "
+                         "arguments, map with (i, j) compiled in, G stored in LDS, or the "
+                         "library's choice")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target host time of the CPU-baseline sample")
@@ -129,7 +139,15 @@ def copy_calibration(steps: int):
                       "ms_per_copy": dt * 1e3, "GBps": 8 * n / dt / 1e9}), flush=True)
 
 
-def make_call(w, inputs, policy):
+def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO):
+    if w.kind == "givens":
+        c, s, B = inputs
+        C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
+        i, j = w.plane
+
+        def call():
+            pkg.givens_emu_batched(i, j, c, s, B, C, mode=givens_mode)
+        return call, C
     if w.kind == "householder":
         u, B = inputs
         C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
@@ -154,7 +172,17 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
     import oracle
 
     threads = oracle.num_threads()
-    if w.kind == "householder":
+    if w.kind == "givens":
+        c, s, B = host_inputs
+        cn, sn, Bn = c.numpy(), s.numpy(), B.numpy()
+        i, j = w.plane
+
+        def run(items):
+            return oracle.givens(i, j, cn, sn, Bn, items=items, want=("c32",))
+
+        def ref(items):
+            return oracle.givens(i, j, cn, sn, Bn, items=items, want=("c64", "n64", "c32"))
+    elif w.kind == "householder":
         u, B = host_inputs
         un, Bn = u.numpy(), B.numpy()
 
@@ -259,7 +287,8 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     policy = None
     if (args.flow, args.ec, args.tile) != (pkg.FLOW_AUTO, 1, pkg.TILE_AUTO):
         policy = pkg.Policy(args.flow, args.ec, args.tile)
-    call, C = make_call(w, dev_inputs, policy)
+    givens_mode = GIVENS_MODES[args.givens_mode]
+    call, C = make_call(w, dev_inputs, policy, givens_mode)
 
     for _ in range(args.warmup):
         call()
@@ -294,7 +323,9 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     resolved, kernel = None, "householder64_kernel"
-    if w.kind == "gemm":
+    if w.kind == "givens":
+        kernel = "givens64_lds_kernel" if givens_mode == pkg.GIVENS_LDS else "givens64_kernel"
+    elif w.kind == "gemm":
         A, B = dev_inputs
         resolved, kernel = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
     roof["kernel"] = kernel
@@ -317,7 +348,9 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
                    "k": w.k, "dist": w.dist, "seed": w.seed,
                    "policy": None if resolved is None else
                    {"flow": resolved.flow, "ec": resolved.ec, "tile": resolved.tile,
-                    "requested": "auto" if policy is None else "explicit"}},
+                    "requested": "auto" if policy is None else "explicit"},
+                   **({"givens": {"plane": list(w.plane), "mode": args.givens_mode}}
+                      if w.kind == "givens" else {})},
         "frac_fp32_vector_peak": tflops / PEAK_FP32_VECTOR_TFLOPS,
         "frac_fp16_mfma_over_3": tflops / (PEAK_FP16_MFMA_TFLOPS / 3),
         "hbm_GBps_algorithmic": bytes_alg / (ms_step * 1e-3) / 1e9,

@@ -183,6 +183,46 @@ int householder_emu_batched(int n, const float* u, int64_t stride_u,
                             int batch, hipStream_t stream);
 
 /*
+ * Batched Givens rotation with the rotation matrix built in registers
+ * (Sec. 4.3.1):
+ *   for t in [0, batch):  C_t := G(i, j, theta_t) . B_t
+ * where G(i, j, theta) is the n x n identity except G_ii = G_jj = c,
+ * G_ij = -s and G_ji = s, with c = cos theta_t and s = sin theta_t given as
+ * c_t = c[t*stride_cs], s_t = s[t*stride_cs] (FP32, used as given: c^2 + s^2
+ * need not be 1).  B_t = B + t*stride_b (n x ncols, row-major, ldb >=
+ * max(1, ncols)), C_t = C + t*stride_c (n x ncols, ldc >= max(1, ncols)).
+ * The plane (i, j) is the same for every item; 0 <= i, j < n, i != j.
+ * The product is formed densely with the emulated FP32 method, as for
+ * sgemm_emu_batched, with G's operand fragments built without memory
+ * traffic.  mode selects how (Sec. 4.3.1 compares these):
+ *   SGEMM_EMU_GIVENS_AUTO      EMBEDDED when (i, j) has a compiled
+ *                              instance, else MAP.
+ *   SGEMM_EMU_GIVENS_MAP       fragments zero-filled, then 1, c, s and -s
+ *                              set through the element map with (i, j)
+ *                              passed as kernel arguments.
+ *   SGEMM_EMU_GIVENS_EMBEDDED  as MAP with (i, j) fixed at compile time;
+ *                              compiled for n = 64 and (i, j) in
+ *                              {(5,37), (37,5), (0,1), (31,32), (62,63)};
+ *                              other planes give SGEMM_EMU_ERR_UNSUPPORTED.
+ *   SGEMM_EMU_GIVENS_LDS       baseline: each wave writes G to LDS and
+ *                              loads its fragments from there.
+ * Supported: n == 64 and ldb < 2^27 (else SGEMM_EMU_ERR_UNSUPPORTED).
+ * Errors: SGEMM_EMU_ERR_DIM (also i or j out of range or i == j), _LD,
+ * _NULL, _STRIDE, _ALIAS (C overlaps B, c or s), _UNSUPPORTED, _POLICY
+ * (unknown mode), _HIP.
+ */
+#define SGEMM_EMU_GIVENS_AUTO 0
+#define SGEMM_EMU_GIVENS_MAP 1
+#define SGEMM_EMU_GIVENS_EMBEDDED 2
+#define SGEMM_EMU_GIVENS_LDS 3
+
+int givens_emu_batched(int n, int i, int j,
+                       const float* c, const float* s, int64_t stride_cs,
+                       const float* B, int ldb, int64_t stride_b, int ncols,
+                       float* C, int ldc, int64_t stride_c,
+                       int batch, int mode, hipStream_t stream);
+
+/*
  * The split of Sec. 4.4 (eqs. corr-1/corr-2) applied elementwise on the
  * device: hi[i], lo[i] receive the binary16 bit patterns of
  * toFP16(x[i]) and toFP16((x[i] - toFP32(hi)) * 2^11).  count >= 0; x, hi

@@ -19,8 +19,10 @@ import os
 __all__ = [
     "SgemmEmuError", "lib_path", "load",
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
-    "householder_emu_batched", "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
-    "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+    "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
+    "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
+    "sgemm_emu_last_hip_error",
+    "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
     "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128", "TILE_128x256",
     "SHAPE_16x16x32", "SHAPE_32x32x16", "USE_A", "USE_B", "USE_ACC",
@@ -34,12 +36,14 @@ FLOW_AUTO, FLOW_SPLIT, FLOW_DIRECT, FLOW_STAGED, FLOW_REG = 0, 1, 2, 3, 4
 TILE_AUTO, TILE_64x64, TILE_128x128, TILE_256x128, TILE_128x256 = 0, 1, 2, 3, 4
 SHAPE_16x16x32, SHAPE_32x32x16 = 0, 1
 USE_A, USE_B, USE_ACC = 0, 1, 2
+GIVENS_AUTO, GIVENS_MAP, GIVENS_EMBEDDED, GIVENS_LDS = 0, 1, 2, 3
 
 # Every symbol declared in include/sgemm_emu.h.
 EXPORTED_SYMBOLS = (
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
-    "householder_emu_batched", "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach",
-    "mfmae_mma_probe", "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+    "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
+    "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
+    "sgemm_emu_last_hip_error",
 )
 
 
@@ -92,6 +96,8 @@ def load():
                                       ctypes.POINTER(Policy), ctypes.POINTER(Policy),
                                       ctypes.POINTER(ctypes.c_char_p)], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
+        "givens_emu_batched": ([i32, i32, i32, P, P, i64, P, i32, i64, i32, P, i32, i64, i32,
+                                i32, P], i32),
         "sgemm_emu_split": ([i64, P, P, P, P], i32),
         "mfmae_num_elements": ([i32, i32], i32),
         "mfmae_map": ([i32, i32, i32, i32, ip, ip], i32),
@@ -242,6 +248,30 @@ def householder_emu_batched(u, B, C=None, *, stream=None):
     rc = load().householder_emu_batched(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C), ldc,
                                         sc, batch, _stream(stream))
     _check(rc, "householder_emu_batched")
+    return C
+
+
+def givens_emu_batched(i, j, c, s, B, C=None, *, mode: int = GIVENS_AUTO, stream=None):
+    """C[t] := G(i, j, theta_t) @ B[t] with c[t] = cos theta_t, s[t] = sin theta_t;
+    c, s: [batch] float32, B: [batch, n, ncols]."""
+    import torch
+
+    for name, v in (("c", c), ("s", s)):
+        if v.dtype != torch.float32 or not v.is_cuda or v.dim() != 1:
+            raise ValueError(f"{name} must be a [batch] float32 device tensor")
+    if c.shape != s.shape or c.stride() != s.stride():
+        raise ValueError("c and s must have the same shape and stride")
+    batch = c.shape[0]
+    bb, n, ncols, ldb, sb = _matrix_view(B, "B")
+    if (bb or 1) != batch:
+        raise ValueError("B must be [batch, n, ncols]")
+    if C is None:
+        C = torch.empty((batch, n, ncols), dtype=torch.float32, device=B.device)
+    _, _, _, ldc, sc = _matrix_view(C, "C")
+    scs = c.stride(0) if batch > 1 else 0
+    rc = load().givens_emu_batched(n, int(i), int(j), _ptr(c), _ptr(s), scs, _ptr(B), ldb, sb,
+                                   ncols, _ptr(C), ldc, sc, batch, int(mode), _stream(stream))
+    _check(rc, "givens_emu_batched")
     return C
 
 

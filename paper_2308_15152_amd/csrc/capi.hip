@@ -275,6 +275,48 @@ int householder_emu_batched(int n, const float* u, int64_t stride_u, const float
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
+int givens_emu_batched(int n, int i, int j, const float* c, const float* s, int64_t stride_cs,
+                       const float* B, int ldb, int64_t stride_b, int ncols, float* C, int ldc,
+                       int64_t stride_c, int batch, int mode, hipStream_t stream) {
+    if (n < 0 || ncols < 0 || batch < 0) return SGEMM_EMU_ERR_DIM;
+    if (mode < SGEMM_EMU_GIVENS_AUTO || mode > SGEMM_EMU_GIVENS_LDS) return SGEMM_EMU_ERR_POLICY;
+    if (ldb < (ncols > 1 ? ncols : 1) || ldc < (ncols > 1 ? ncols : 1)) return SGEMM_EMU_ERR_LD;
+    if (n == 0 || ncols == 0 || batch == 0) return SGEMM_EMU_OK;
+    if (i < 0 || j < 0 || i >= n || j >= n || i == j) return SGEMM_EMU_ERR_DIM;
+    if (n != 64) return SGEMM_EMU_ERR_UNSUPPORTED;
+    // the kernel forms 8 * ldb + column as a 32-bit lane offset
+    if (ldb >= (1 << 27)) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (mode == SGEMM_EMU_GIVENS_AUTO)
+        mode = sgemm_emu::givens_embedded(i, j) ? SGEMM_EMU_GIVENS_EMBEDDED : SGEMM_EMU_GIVENS_MAP;
+    if (mode == SGEMM_EMU_GIVENS_EMBEDDED && !sgemm_emu::givens_embedded(i, j))
+        return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (c == nullptr || s == nullptr || B == nullptr || C == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (stride_cs < 0 || stride_b < 0 || stride_c < 0) return SGEMM_EMU_ERR_STRIDE;
+    if (batch > 1 && stride_c < (int64_t)(n - 1) * ldc + ncols) return SGEMM_EMU_ERR_STRIDE;
+    const Extent ec = extent(C, batch, n, ncols, ldc, stride_c);
+    const Extent ecs = extent(c, stride_cs == 0 ? 1 : batch, 1, 1, 1, stride_cs);
+    const Extent ess = extent(s, stride_cs == 0 ? 1 : batch, 1, 1, 1, stride_cs);
+    const Extent eb = extent(B, stride_b == 0 ? 1 : batch, n, ncols, ldb, stride_b);
+    if (overlap(ec, ecs) || overlap(ec, ess) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
+    sgemm_emu::GivensArgs a;
+    a.ncols = ncols;
+    a.i = i;
+    a.j = j;
+    a.c = c;
+    a.s = s;
+    a.scs = stride_cs;
+    a.B = B;
+    a.ldb = ldb;
+    a.sb = stride_b;
+    a.C = C;
+    a.ldc = ldc;
+    a.sc = stride_c;
+    a.batch = batch;
+    a.mode = mode;
+    hipError_t e = sgemm_emu::launch_givens64(a, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
 int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                     hipStream_t stream) {
     if (count < 0) return SGEMM_EMU_ERR_DIM;

@@ -50,6 +50,24 @@ struct HouseholderArgs {
 
 hipError_t launch_householder64(const HouseholderArgs& a, hipStream_t stream);
 
+struct GivensArgs {
+    int ncols;
+    int i, j;  // rotation plane
+    const float* c;
+    const float* s;
+    int64_t scs;
+    const float* B;
+    int64_t ldb, sb;
+    float* C;
+    int64_t ldc, sc;
+    int batch;
+    int mode;  // SGEMM_EMU_GIVENS_MAP, _EMBEDDED or _LDS (resolved, not AUTO)
+};
+
+// True if the plane (i, j) of n = 64 has a compile-time kernel instance.
+bool givens_embedded(int i, int j);
+hipError_t launch_givens64(const GivensArgs& a, hipStream_t stream);
+
 hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                         hipStream_t stream);
 

@@ -210,6 +210,48 @@ def test_householder_validation():
     assert hh(ncols=0) == 0
 
 
+def test_givens_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    PS = PA + 0x100000
+
+    def gv(n=64, i=5, j=37, c=PA, s=PS, scs=1, B=PB, ldb=64, sb=4096, ncols=64, C=PC, ldc=64,
+           sc=4096, batch=2, mode=0):
+        return lib.givens_emu_batched(n, i, j, P(c), P(s), scs, P(B), ldb, sb, ncols, P(C), ldc,
+                                      sc, batch, mode, P(0))
+
+    assert gv(n=-1) == -1
+    assert gv(ncols=-1) == -1
+    assert gv(batch=-1) == -1
+    assert gv(i=64) == -1
+    assert gv(j=-1) == -1
+    assert gv(i=7, j=7) == -1
+    assert gv(mode=4) == -8
+    assert gv(mode=-1) == -8
+    assert gv(ldb=63) == -2
+    assert gv(ldc=10) == -2
+    assert gv(n=32, i=1, j=2) == -6
+    assert gv(ldb=1 << 27, sb=1 << 33) == -6
+    # (3, 60) has no compile-time instance: EMBEDDED refuses it, AUTO and the
+    # other modes accept it (checked up to the first pointer test)
+    assert gv(i=3, j=60, mode=2) == -6
+    assert gv(i=3, j=60, mode=0, c=0) == -3
+    assert gv(i=3, j=60, mode=1, c=0) == -3
+    assert gv(i=37, j=5, mode=2, c=0) == -3
+    assert gv(s=0) == -3
+    assert gv(B=0) == -3
+    assert gv(C=0) == -3
+    assert gv(scs=-1) == -4
+    assert gv(sb=-1) == -4
+    assert gv(sc=100) == -4
+    assert gv(C=PB) == -5
+    assert gv(C=PA - 4) == -5
+    assert gv(C=PS - 64 * 64 * 4 + 8) == -5
+    assert gv(batch=0) == 0
+    assert gv(ncols=0) == 0
+    assert gv(n=0) == 0
+
+
 def test_split_validation():
     lib = pkg.load()
     P = ctypes.c_void_p
