@@ -19,6 +19,9 @@ it follows:
   inputs, the normaliser sum_k |a||b|, the plain FP32 product (sequential
   fmaf chain, ascending k) and the method-exact model of eq. corr-5 summed in
   FP64.
+* :func:`gemm_acc` -- D = op(A).op(B) + C (op: as stored or transposed),
+  the multiply-accumulate form of a fragment API (Sec. 2.2, Sec. 4.4): the
+  same four quantities with C as the first term of every sum.
 * :func:`householder` -- H = I - 2 u u^T formed explicitly and applied to B
   (Sec. 4.2.1, eq. householder, read as an outer product of u).
 * :func:`givens_matrix`, :func:`givens` -- the rotation G(i, j, theta) of
@@ -62,6 +65,9 @@ def _load():
     lib.oracle_gemm.argtypes = [i32, i32, i32, i32, P, i64, i64, P, i64, i64,
                                 P, P, P, P, i64, i64]
     lib.oracle_gemm.restype = None
+    lib.oracle_gemm_acc.argtypes = [i32, i32, i32, i32, P, i64, i64, P, i64, i64,
+                                     P, i64, i64, P, P, P, P, i64, i64]
+    lib.oracle_gemm_acc.restype = None
     lib.oracle_dots.argtypes = [i64, i32, P, P, P, P, P, P]
     lib.oracle_dots.restype = None
     lib.oracle_householder_h32.argtypes = [i32, P, P]
@@ -156,6 +162,38 @@ def gemm(A: np.ndarray, B: np.ndarray, want=("c64", "n64", "c32", "cm")):
     _load().oracle_gemm(batch, m, n, k, _ptr(A), k, m * k, _ptr(B), n, k * n,
                         _ptr(out["c64"]), _ptr(out["n64"]), _ptr(out["c32"]),
                         _ptr(out["cm"]), n, m * n)
+    return {key: v for key, v in out.items() if v is not None}
+
+
+def gemm_acc(A: np.ndarray, B: np.ndarray, C: np.ndarray, op_a: str = "N", op_b: str = "N",
+             want=("c64", "n64", "c32", "cm")):
+    """Oracle quantities for D = op(A).op(B) + C over a batch.
+
+    A is stored as [batch, m, k] (op_a "N") or [batch, k, m] (op_a "T", A is
+    its transpose); B as [batch, k, n] ("N") or [batch, n, k] ("T"); C is
+    [batch, m, n].  Transposed operands are copied into row-major form
+    first; the arithmetic is the same as for "N"."""
+    A = np.asarray(A, dtype=np.float32)
+    B = np.asarray(B, dtype=np.float32)
+    C = _f32(C)
+    if A.ndim == 2:
+        A = A[None]
+    if B.ndim == 2:
+        B = B[None]
+    if C.ndim == 2:
+        C = C[None]
+    A = _f32(A.transpose(0, 2, 1) if op_a == "T" else A)
+    B = _f32(B.transpose(0, 2, 1) if op_b == "T" else B)
+    batch, m, k = A.shape
+    n = B.shape[2]
+    assert B.shape == (batch, k, n) and C.shape == (batch, m, n)
+    out = {}
+    for key, dt in (("c64", np.float64), ("n64", np.float64),
+                    ("c32", np.float32), ("cm", np.float64)):
+        out[key] = np.zeros((batch, m, n), dtype=dt) if key in want else None
+    _load().oracle_gemm_acc(batch, m, n, k, _ptr(A), k, m * k, _ptr(B), n, k * n,
+                            _ptr(C), n, m * n, _ptr(out["c64"]), _ptr(out["n64"]),
+                            _ptr(out["c32"]), _ptr(out["cm"]), n, m * n)
     return {key: v for key, v in out.items() if v is not None}
 
 

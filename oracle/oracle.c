@@ -23,6 +23,8 @@
  *     compared with, Sec. 4.4 and 4.4.2), and the method-exact model
  *     A_F16 B_F16 + (dA_F16 B_F16 + A_F16 dB_F16) / 2^11 summed in FP64
  *     (Sec. 4.4, eq. corr-5).
+ *   - oracle_gemm_acc: the accumulate form D = A*B + C0 of a fragment API
+ *     (Sec. 2.2, Sec. 4.4), the same quantities with C0 as every sum's start.
  *   - oracle_householder: H = I - 2 u u^T built explicitly and applied to
  *     B (Sec. 4.2.1, eq. householder, read as an outer product).
  *   - oracle_givens: the rotation G(i, j, theta) of Sec. 4.3.1 (identity
@@ -201,6 +203,63 @@ void oracle_gemm(int batch, int m, int n, int k,
                 }
             }
             int64_t o = b * sc + i * ldc + j;
+            if (C64)
+                C64[o] = s64;
+            if (N64)
+                N64[o] = nrm;
+            if (C32)
+                C32[o] = s32;
+            if (CM)
+                CM[o] = sm;
+        }
+    }
+}
+
+/* Accumulate form D = A * B + C0 (the matrix-multiply-accumulate of a
+ * fragment API, Sec. 2.2 and Sec. 4.4): the same four quantities as
+ * oracle_gemm with C0 as the starting value of every sum,
+ *   C64 = C0 + sum_k A B          (FP64, C0 first, then k ascending)
+ *   N64 = |C0| + sum_k |A| |B|
+ *   C32: c = C0; for k ascending: c = fmaf(A, B, c)
+ *   CM  = C0 + sum_k [ hiA hiB + (loA hiB + hiA loB) * 2^-11 ]  (FP64)
+ * C0 has row stride ldc0 and item stride sc0; outputs ldd and sd. */
+void oracle_gemm_acc(int batch, int m, int n, int k,
+                     const float *A, int64_t lda, int64_t sa,
+                     const float *B, int64_t ldb, int64_t sb,
+                     const float *C0, int64_t ldc0, int64_t sc0,
+                     double *C64, double *N64, float *C32, double *CM,
+                     int64_t ldd, int64_t sd)
+{
+    int64_t rows = (int64_t)batch * m;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < rows; ++r) {
+        int64_t b = r / m, i = r % m;
+        const float *a = A + b * sa + i * lda;
+        const float *bb = B + b * sb;
+        const float *c0 = C0 + b * sc0 + i * ldc0;
+        for (int j = 0; j < n; ++j) {
+            float cv = c0[j];
+            double s64 = cv, nrm = fabs((double)cv), sm = cv;
+            float s32 = cv;
+            for (int kk = 0; kk < k; ++kk) {
+                float av = a[kk];
+                float bv = bb[(int64_t)kk * ldb + j];
+                s64 += (double)av * (double)bv;
+                nrm += fabs((double)av) * fabs((double)bv);
+                s32 = fmaf(av, bv, s32);
+                if (CM) {
+                    uint16_t ha = oracle_f32_to_f16(av);
+                    uint16_t hb = oracle_f32_to_f16(bv);
+                    double ah = oracle_f16_to_f32(ha);
+                    double bh = oracle_f16_to_f32(hb);
+                    double al = oracle_f16_to_f32(oracle_f32_to_f16(
+                        (av - (float)ah) * 2048.0f));
+                    double bl = oracle_f16_to_f32(oracle_f32_to_f16(
+                        (bv - (float)bh) * 2048.0f));
+                    sm += ah * bh + (al * bh + ah * bl) / 2048.0;
+                }
+            }
+            int64_t o = b * sd + i * ldd + j;
             if (C64)
                 C64[o] = s64;
             if (N64)
