@@ -26,10 +26,12 @@ to scale the HBM traffic counters of a profiler run.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -60,18 +62,31 @@ KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are ad
     "householder64_kernel": "rulebuilt.hip",
     "givens64_kernel": "rulebuilt.hip",
     "givens64_lds_kernel": "rulebuilt.hip",
+    "gemm_acc_kernel": "gemm_acc.hip",
 }
 
 
 def kernel_source_hash(kernel: str) -> str:
     """SHA-256 over the sources a kernel is built from: its translation unit
-    and every header."""
+    and every header it includes (transitively, quoted includes found in the
+    package's csrc/ or in include/)."""
     csrc = os.path.join(ROOT, "paper_2308_15152_amd", "csrc")
-    files = sorted([os.path.join(csrc, KERNEL_SOURCES[kernel])] +
-                   glob.glob(os.path.join(csrc, "*.h*")) +
-                   glob.glob(os.path.join(ROOT, "include", "**", "*.h*"), recursive=True))
+    inc = os.path.join(ROOT, "include")
+    seen, todo = set(), [os.path.join(csrc, KERNEL_SOURCES[kernel])]
+    while todo:
+        f = todo.pop()
+        if f in seen:
+            continue
+        seen.add(f)
+        with open(f) as fh:
+            for name in re.findall(r'^\s*#\s*include\s+"([^"]+)"', fh.read(), flags=re.M):
+                for d in (os.path.dirname(f), csrc, inc):
+                    cand = os.path.normpath(os.path.join(d, name))
+                    if os.path.exists(cand):
+                        todo.append(cand)
+                        break
     h = hashlib.sha256()
-    for f in files:
+    for f in sorted(seen):
         h.update(os.path.relpath(f, ROOT).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())
@@ -112,6 +127,9 @@ def parse():
                     help="how a Givens workload builds G: map with (i, j) as kernel "
                          "arguments, map with (i, j) compiled in, G stored in LDS, or the "
                          "library's choice")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="override the workload's batch size (a measurement variant, "
+                         "recorded in config; the default line uses the workload's own)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target host time of the CPU-baseline sample")
@@ -148,6 +166,13 @@ def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO):
         def call():
             pkg.givens_emu_batched(i, j, c, s, B, C, mode=givens_mode)
         return call, C
+    if w.kind == "gemm_acc":
+        At, B, Cin = inputs
+        D = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
+
+        def call():
+            pkg.sgemm_emu_batched_acc(At, B, Cin, D, op_a=pkg.OP_T)
+        return call, D
     if w.kind == "householder":
         u, B = inputs
         C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
@@ -182,6 +207,16 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
 
         def ref(items):
             return oracle.givens(i, j, cn, sn, Bn, items=items, want=("c64", "n64", "c32"))
+    elif w.kind == "gemm_acc":
+        At, B, Cin = host_inputs
+
+        def run(items):
+            return oracle.gemm_acc(At[items].numpy(), B[items].numpy(), Cin[items].numpy(),
+                                   "T", "N", want=("c32",))
+
+        def ref(items):
+            return oracle.gemm_acc(At[items].numpy(), B[items].numpy(), Cin[items].numpy(),
+                                   "T", "N", want=("c64", "n64", "c32"))
     elif w.kind == "householder":
         u, B = host_inputs
         un, Bn = u.numpy(), B.numpy()
@@ -282,6 +317,8 @@ def main():
 def bench_workload(args, name: str, cpu: bool) -> dict:
     """Time one workload; the JSON record of the benchmark contract."""
     w = synth.WORKLOADS[name]
+    if args.batch is not None and args.batch != w.batch:
+        w = dataclasses.replace(w, batch=args.batch)
     host_inputs = synth.workload_inputs(w)
     dev_inputs = tuple(t.to("cuda") for t in host_inputs)
     policy = None
@@ -325,11 +362,18 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     resolved, kernel = None, "householder64_kernel"
     if w.kind == "givens":
         kernel = "givens64_lds_kernel" if givens_mode == pkg.GIVENS_LDS else "givens64_kernel"
+    elif w.kind == "gemm_acc":
+        kernel = "gemm_acc_kernel"
     elif w.kind == "gemm":
         A, B = dev_inputs
         resolved, kernel = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
     roof["kernel"] = kernel
-    roof["traffic"] = measured_traffic(w.name, roof["kernel"])
+    tkey = w.name
+    if w.kind == "givens" and args.givens_mode != "auto":
+        tkey += ":" + args.givens_mode
+    if w.batch != synth.WORKLOADS[name].batch:
+        tkey += f":batch{w.batch}"
+    roof["traffic"] = measured_traffic(tkey, roof["kernel"])
 
     out = {
         "metric": METRIC,

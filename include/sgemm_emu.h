@@ -166,6 +166,52 @@ int sgemm_emu_resolve_policy(int m, int n, int k,
                              const char** kernel);
 
 /*
+ * Batched multiply-accumulate in emulated FP32 with transposable operands:
+ *   for t in [0, batch):  D_t := op(A_t) . op(B_t) + C_t
+ * the matrix-multiply-accumulate of a fragment API (Sec. 2.2) computed by
+ * the method of Sec. 4.4 through the library's fragment interface
+ * (mfmae/wmma_tcec.hpp; the kernel is written with its load_matrix_sync,
+ * mma_sync and store_matrix_sync).  op(A) is m x k, op(B) is k x n.
+ *   op_a: SGEMM_EMU_OP_N  A_t is stored m x k row-major, lda >= max(1, k)
+ *         SGEMM_EMU_OP_T  A_t is stored as its transpose, k x m row-major
+ *                         (A column-major), lda >= max(1, m)
+ *   op_b: SGEMM_EMU_OP_N  B_t stored k x n row-major, ldb >= max(1, n)
+ *         SGEMM_EMU_OP_T  B_t stored n x k row-major, ldb >= max(1, k)
+ *   layout_cd: SGEMM_EMU_ROW_MAJOR  C_t and D_t are m x n row-major,
+ *                                   ldc, ldd >= max(1, n)
+ *              SGEMM_EMU_COL_MAJOR  stored as n x m row-major,
+ *                                   ldc, ldd >= max(1, m)
+ * A_t = A + t*stride.a, B_t = B + t*stride.b, C_t = C + t*stride.c,
+ * D_t = D + t*stride.d.  C may be NULL (then D := op(A).op(B)); C == D with
+ * ldc == ldd and stride.c == stride.d accumulates in place; any other
+ * overlap of D with A, B or C is an error.  k = 0 gives D := C (or 0).
+ * shape selects the instruction (MFMAE_SHAPE_16x16x32 or
+ * MFMAE_SHAPE_32x32x16), ec the policy: 1 = error correction (3 products),
+ * 0 = hi.hi only.  16-byte accesses are used along each operand's contiguous
+ * direction when its base is 16-byte aligned and its ld and stride are
+ * multiples of 4; any alignment is accepted.
+ * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL (A or B NULL with k > 0, D NULL),
+ * _STRIDE, _ALIAS, _POLICY (op, layout, shape or ec out of range), _HIP.
+ */
+#define SGEMM_EMU_OP_N 0
+#define SGEMM_EMU_OP_T 1
+#define SGEMM_EMU_ROW_MAJOR 0
+#define SGEMM_EMU_COL_MAJOR 1
+
+typedef struct {
+    int64_t a, b, c, d;
+} sgemm_emu_stride4_t;
+
+int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd,
+                          int m, int n, int k,
+                          const float* A, int lda,
+                          const float* B, int ldb,
+                          const float* C, int ldc,
+                          float* D, int ldd,
+                          int batch, sgemm_emu_stride4_t stride,
+                          int shape, int ec, hipStream_t stream);
+
+/*
  * Batched Householder application with the reflector built in registers
  * (Sec. 4.2.1, eq. householder, read as H = I - 2 u u^T):
  *   for t in [0, batch):  C_t := (I - 2 u_t u_t^T) . B_t

@@ -19,9 +19,11 @@ import os
 __all__ = [
     "SgemmEmuError", "lib_path", "load",
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
+    "sgemm_emu_batched_acc",
     "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
     "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
     "sgemm_emu_last_hip_error",
+    "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
     "TILE_AUTO", "TILE_64x64", "TILE_128x128", "TILE_256x128", "TILE_128x256",
@@ -37,10 +39,13 @@ TILE_AUTO, TILE_64x64, TILE_128x128, TILE_256x128, TILE_128x256 = 0, 1, 2, 3, 4
 SHAPE_16x16x32, SHAPE_32x32x16 = 0, 1
 USE_A, USE_B, USE_ACC = 0, 1, 2
 GIVENS_AUTO, GIVENS_MAP, GIVENS_EMBEDDED, GIVENS_LDS = 0, 1, 2, 3
+OP_N, OP_T = 0, 1
+ROW_MAJOR, COL_MAJOR = 0, 1
 
 # Every symbol declared in include/sgemm_emu.h.
 EXPORTED_SYMBOLS = (
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
+    "sgemm_emu_batched_acc",
     "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
     "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
     "sgemm_emu_last_hip_error",
@@ -58,6 +63,11 @@ class SgemmEmuError(RuntimeError):
 
 class Stride(ctypes.Structure):
     _fields_ = [("a", ctypes.c_int64), ("b", ctypes.c_int64), ("c", ctypes.c_int64)]
+
+
+class Stride4(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_int64), ("b", ctypes.c_int64), ("c", ctypes.c_int64),
+                ("d", ctypes.c_int64)]
 
 
 class Policy(ctypes.Structure):
@@ -95,6 +105,8 @@ def load():
         "sgemm_emu_resolve_policy": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride,
                                       ctypes.POINTER(Policy), ctypes.POINTER(Policy),
                                       ctypes.POINTER(ctypes.c_char_p)], i32),
+        "sgemm_emu_batched_acc": ([i32, i32, i32, i32, i32, i32, P, i32, P, i32, P, i32, P, i32,
+                                   i32, Stride4, i32, i32, P], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
         "givens_emu_batched": ([i32, i32, i32, P, P, i64, P, i32, i64, i32, P, i32, i64, i32,
                                 i32, P], i32),
@@ -227,6 +239,48 @@ def sgemm_emu_resolve_policy(A, B, C, *, policy: Policy | None = None):
 
 def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):
     return sgemm_emu_batched(A, B, C, policy=policy, stream=stream)
+
+
+def sgemm_emu_batched_acc(A, B, C=None, D=None, *, op_a: int = OP_N, op_b: int = OP_N,
+                          layout: int = ROW_MAJOR, shape: int = SHAPE_32x32x16, ec: int = 1,
+                          stream=None):
+    """D := op(A) @ op(B) + C per batch item.
+
+    A, B, C, D are 2-D or 3-D float32 device tensors with contiguous rows,
+    given in their stored form: A is [m, k] (op_a OP_N) or [k, m] (OP_T),
+    B is [k, n] or [n, k]; C and D are [m, n] (layout ROW_MAJOR) or [n, m]
+    (COL_MAJOR).  C may be None (zero) or D itself (in place); D is
+    allocated if None."""
+    import torch
+
+    ba, ar, ac, lda, sa = _matrix_view(A, "A")
+    bb, br, bc, ldb, sb = _matrix_view(B, "B")
+    m, k = (ac, ar) if op_a == OP_T else (ar, ac)
+    kb, n = (bc, br) if op_b == OP_T else (br, bc)
+    if kb != k:
+        raise ValueError(f"inner dimensions differ: {k} vs {kb}")
+    batch = max(ba or 1, bb or 1)
+    for name, b in (("A", ba), ("B", bb)):
+        if b is not None and b != batch:
+            raise ValueError(f"{name} batch {b} != {batch}")
+    stored = (n, m) if layout == COL_MAJOR else (m, n)
+    if D is None:
+        shape_d = (batch, *stored) if (ba is not None or bb is not None) else stored
+        D = torch.empty(shape_d, dtype=torch.float32, device=A.device)
+    bd, dr, dc, ldd, sd = _matrix_view(D, "D")
+    if (dr, dc) != stored or (bd or 1) != batch:
+        raise ValueError("D has the wrong shape")
+    ldc, sc = 1, 0
+    if C is not None:
+        bcx, cr, ccol, ldc, sc = _matrix_view(C, "C")
+        if (cr, ccol) != stored or (bcx is not None and bcx != batch):
+            raise ValueError("C has the wrong shape")
+    st = Stride4(sa, sb, sc, sd)
+    rc = load().sgemm_emu_batched_acc(int(op_a), int(op_b), int(layout), m, n, k, _ptr(A), lda,
+                                      _ptr(B), ldb, _ptr(C), ldc, _ptr(D), ldd, batch, st,
+                                      int(shape), int(ec), _stream(stream))
+    _check(rc, "sgemm_emu_batched_acc")
+    return D
 
 
 def householder_emu_batched(u, B, C=None, *, stream=None):

@@ -244,6 +244,71 @@ int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const
     return SGEMM_EMU_OK;
 }
 
+int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k, const float* A,
+                          int lda, const float* B, int ldb, const float* C, int ldc, float* D,
+                          int ldd, int batch, sgemm_emu_stride4_t stride, int shape, int ec,
+                          hipStream_t stream) {
+    if ((op_a != SGEMM_EMU_OP_N && op_a != SGEMM_EMU_OP_T) ||
+        (op_b != SGEMM_EMU_OP_N && op_b != SGEMM_EMU_OP_T) ||
+        (layout_cd != SGEMM_EMU_ROW_MAJOR && layout_cd != SGEMM_EMU_COL_MAJOR) ||
+        (shape != MFMAE_SHAPE_16x16x32 && shape != MFMAE_SHAPE_32x32x16) || (ec != 0 && ec != 1))
+        return SGEMM_EMU_ERR_POLICY;
+    if (m < 0 || n < 0 || k < 0 || batch < 0) return SGEMM_EMU_ERR_DIM;
+    const bool at = op_a == SGEMM_EMU_OP_T, bt = op_b == SGEMM_EMU_OP_T;
+    const bool cdc = layout_cd == SGEMM_EMU_COL_MAJOR;
+    // stored shapes (rows x cols, row-major with the given ld)
+    const int ar = at ? k : m, ac = at ? m : k;
+    const int br = bt ? n : k, bc = bt ? k : n;
+    const int cr = cdc ? n : m, cc = cdc ? m : n;
+    auto ld_ok = [](int ld, int cols) { return ld >= (cols > 1 ? cols : 1); };
+    if (!ld_ok(lda, ac) || !ld_ok(ldb, bc) || !ld_ok(ldd, cc) || (C && !ld_ok(ldc, cc)))
+        return SGEMM_EMU_ERR_LD;
+    if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
+    if (D == nullptr || (k > 0 && (A == nullptr || B == nullptr))) return SGEMM_EMU_ERR_NULL;
+    if (stride.a < 0 || stride.b < 0 || stride.c < 0 || stride.d < 0) return SGEMM_EMU_ERR_STRIDE;
+    if (batch > 1 && stride.d < (int64_t)(cr - 1) * ldd + cc) return SGEMM_EMU_ERR_STRIDE;
+    const Extent ed = extent(D, batch, cr, cc, ldd, stride.d);
+    const Extent ea = k > 0 ? extent(A, stride.a == 0 ? 1 : batch, ar, ac, lda, stride.a) : Extent{};
+    const Extent eb = k > 0 ? extent(B, stride.b == 0 ? 1 : batch, br, bc, ldb, stride.b) : Extent{};
+    if (overlap(ed, ea) || overlap(ed, eb)) return SGEMM_EMU_ERR_ALIAS;
+    if (C) {
+        const bool in_place = C == D && ldc == ldd && stride.c == stride.d;
+        const Extent ecx = extent(C, stride.c == 0 ? 1 : batch, cr, cc, ldc, stride.c);
+        if (!in_place && overlap(ed, ecx)) return SGEMM_EMU_ERR_ALIAS;
+    }
+    auto vec_ok = [](const void* p, int64_t ld, int64_t s) {
+        return ((uintptr_t)p % 16 == 0) && ld % 4 == 0 && s % 4 == 0;
+    };
+    sgemm_emu::AccArgs a;
+    a.m = m;
+    a.n = n;
+    a.k = k;
+    a.A = A;
+    a.lda = lda;
+    a.sa = stride.a;
+    a.B = B;
+    a.ldb = ldb;
+    a.sb = stride.b;
+    a.C = C;
+    a.ldc = ldc;
+    a.sc = stride.c;
+    a.D = D;
+    a.ldd = ldd;
+    a.sd = stride.d;
+    a.batch = batch;
+    a.a_trans = at;
+    a.b_trans = bt;
+    a.cd_col = cdc;
+    // 16-byte accesses happen only along a contiguous direction: A stored
+    // m x k, B stored n x k, C and D stored column-major
+    a.vec_a = at || vec_ok(A, lda, stride.a);
+    a.vec_b = !bt || vec_ok(B, ldb, stride.b);
+    a.vec_c = C == nullptr || !cdc || vec_ok(C, ldc, stride.c);
+    a.vec_d = !cdc || vec_ok(D, ldd, stride.d);
+    hipError_t e = sgemm_emu::launch_gemm_acc(a, shape, ec == 1, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
 int householder_emu_batched(int n, const float* u, int64_t stride_u, const float* B, int ldb,
                             int64_t stride_b, int ncols, float* C, int ldc, int64_t stride_c,
                             int batch, hipStream_t stream) {

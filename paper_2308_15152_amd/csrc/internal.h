@@ -68,6 +68,25 @@ struct GivensArgs {
 bool givens_embedded(int i, int j);
 hipError_t launch_givens64(const GivensArgs& a, hipStream_t stream);
 
+// D = op(A) op(B) + C through the fragment interface (C may be null: zero).
+struct AccArgs {
+    int m, n, k;
+    const float* A;
+    int64_t lda, sa;
+    const float* B;
+    int64_t ldb, sb;
+    const float* C;
+    int64_t ldc, sc;
+    float* D;
+    int64_t ldd, sd;
+    int batch;
+    bool a_trans, b_trans, cd_col;
+    bool vec_a, vec_b, vec_c, vec_d;  // 16-byte accesses legal (contiguous direction)
+};
+
+// shape: 0 = 16x16x32, 1 = 32x32x16.
+hipError_t launch_gemm_acc(const AccArgs& a, int shape, bool ec, hipStream_t stream);
+
 hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                         hipStream_t stream);
 

@@ -20,6 +20,8 @@ Workloads (row-major, contiguous, FP32):
   its FP32 2-norm, B 64 x 64 uniform(-1, 1),                               seed 5
 * ``paper_k<K>``  batch 256, 1024 x 1024 x K for K in PAPER_SWEEP_K,
   entries uniform(-1, 1),                                                  seed 6
+* ``gemm_acc_128``  batch 4096, D = A^T B + C with A stored k x m (128 x 128),
+  B 128 x 128, C 128 x 128, entries uniform(-1, 1), drawn A, B, C,         seed 8
 * ``givens_64``  batch 262144, rotation plane (i, j) = (5, 37) of n = 64,
   theta uniform in [0, 2 pi) per item with c, s = cos, sin theta evaluated
   in FP64 and rounded to FP32, B 64 x 64 uniform(-1, 1),                   seed 7
@@ -37,7 +39,7 @@ import torch
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str        # "gemm", "householder" or "givens"
+    kind: str        # "gemm", "gemm_acc", "householder" or "givens"
     batch: int
     m: int
     n: int
@@ -62,6 +64,9 @@ class Workload:
             per = 4 * (self.m + self.k * self.n + self.m * self.n)
         elif self.kind == "givens":
             per = 4 * (2 + self.k * self.n + self.m * self.n)
+        elif self.kind == "gemm_acc":
+            # read A, B and C, write D
+            per = 4 * (self.m * self.k + self.k * self.n + 2 * self.m * self.n)
         else:
             per = 4 * (self.m * self.k + self.k * self.n + self.m * self.n)
         return per * self.batch
@@ -85,6 +90,7 @@ for _k in PAPER_SWEEP_K:
                                          "uniform", 6)
 
 
+WORKLOADS["gemm_acc_128"] = Workload("gemm_acc_128", "gemm_acc", 4096, 128, 128, 128, "uniform", 8)
 WORKLOADS["givens_64"] = Workload("givens_64", "givens", 262144, 64, 64, 64, "givens", 7,
                                   (5, 37))
 
@@ -128,6 +134,16 @@ def householder_inputs(batch: int, n: int, ncols: int, seed: int):
     return u, B
 
 
+def gemm_acc_inputs(batch: int, m: int, n: int, k: int, seed: int):
+    """For D = A^T B + C: A stored as [batch, k, m], then B [batch, k, n],
+    then C [batch, m, n], all uniform(-1, 1), drawn in that order."""
+    g = _gen(seed)
+    At = uniform((batch, k, m), g)
+    B = uniform((batch, k, n), g)
+    C = uniform((batch, m, n), g)
+    return At, B, C
+
+
 def givens_inputs(batch: int, n: int, ncols: int, seed: int):
     """c [batch], s [batch] (theta uniform in [0, 2 pi), cos and sin in FP64
     rounded to FP32), then B [batch, n, ncols] uniform(-1, 1), drawn in that
@@ -149,6 +165,8 @@ def workload_inputs(w: Workload, batch: int | None = None):
         return householder_inputs(b, w.m, w.n, w.seed)
     if w.kind == "givens":
         return givens_inputs(b, w.m, w.n, w.seed)
+    if w.kind == "gemm_acc":
+        return gemm_acc_inputs(b, w.m, w.n, w.k, w.seed)
     return gemm_inputs(b, w.m, w.n, w.k, w.seed, w.dist)
 
 

@@ -252,6 +252,52 @@ def test_givens_validation():
     assert gv(n=0) == 0
 
 
+def test_batched_acc_validation():
+    """Every call here ends in an error before anything is launched: the
+    cases that pass one check carry a negative stride, which is rejected
+    after the dimension, ld and pointer checks."""
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    PD = PC + 0x1000000
+    BAD = (-1, 0, 0, 64 * 48)  # rejected with -4 after every earlier check
+
+    def acc(op_a=0, op_b=0, lay=0, m=64, n=48, k=32, A=PA, lda=32, B=PB, ldb=48, C=PC, ldc=48,
+            D=PD, ldd=48, batch=2, st=BAD, shape=1, ec=1):
+        return lib.sgemm_emu_batched_acc(op_a, op_b, lay, m, n, k, P(A), lda, P(B), ldb, P(C),
+                                         ldc, P(D), ldd, batch, pkg.Stride4(*st), shape, ec,
+                                         P(0))
+
+    assert acc() == -4
+    for bad in (dict(op_a=2), dict(op_b=-1), dict(lay=2), dict(shape=2), dict(ec=2)):
+        assert acc(**bad) == -8, bad
+    assert acc(m=-1) == -1
+    assert acc(k=-1) == -1
+    assert acc(batch=-1) == -1
+    assert acc(lda=31) == -2
+    assert acc(op_a=1, lda=32) == -2          # A stored k x m needs lda >= m
+    assert acc(op_a=1, lda=64) == -4
+    assert acc(ldb=47) == -2
+    assert acc(op_b=1, ldb=32) == -4          # B stored n x k: ldb >= k
+    assert acc(op_b=1, ldb=31) == -2
+    assert acc(ldd=47) == -2
+    assert acc(ldc=47) == -2
+    assert acc(C=0, ldc=1) == -4              # no C: its ld is not checked
+    assert acc(lay=1) == -2                   # stored n x m: ld >= m
+    assert acc(lay=1, ldc=64, ldd=64) == -4
+    assert acc(m=0) == 0
+    assert acc(batch=0) == 0
+    assert acc(D=0) == -3
+    assert acc(A=0) == -3
+    assert acc(B=0) == -3
+    assert acc(A=0, B=0, k=0) == -4           # k = 0 reads neither
+    ok = (64 * 32, 32 * 48, 64 * 48, 64 * 48)
+    assert acc(st=(0, 0, 0, 100)) == -4       # D items overlap
+    assert acc(st=ok, D=PB + 4) == -5
+    assert acc(st=ok, D=PA) == -5
+    assert acc(st=ok, D=PC + 8) == -5         # partial overlap with C
+    assert acc(st=ok, C=PD, D=PD, ldc=64, ldd=48) == -5
+
+
 def test_split_validation():
     lib = pkg.load()
     P = ctypes.c_void_p
