@@ -22,6 +22,9 @@ it follows:
 * :func:`gemm_acc` -- D = op(A).op(B) + C (op: as stored or transposed),
   the multiply-accumulate form of a fragment API (Sec. 2.2, Sec. 4.4): the
   same four quantities with C as the first term of every sum.
+* :func:`scan` -- inclusive prefix sums of each row: a^T U with U the
+  upper-triangular all-ones matrix of Sec. 4.2 (eq. scan-mat), written as
+  running sums (FP64, |x|, FP32, and the split model).
 * :func:`householder` -- H = I - 2 u u^T formed explicitly and applied to B
   (Sec. 4.2.1, eq. householder, read as an outer product of u).
 * :func:`givens_matrix`, :func:`givens` -- the rotation G(i, j, theta) of
@@ -68,6 +71,8 @@ def _load():
     lib.oracle_gemm_acc.argtypes = [i32, i32, i32, i32, P, i64, i64, P, i64, i64,
                                      P, i64, i64, P, P, P, P, i64, i64]
     lib.oracle_gemm_acc.restype = None
+    lib.oracle_scan.argtypes = [i64, i32, P, i64, P, P, P, P, i64]
+    lib.oracle_scan.restype = None
     lib.oracle_dots.argtypes = [i64, i32, P, P, P, P, P, P]
     lib.oracle_dots.restype = None
     lib.oracle_householder_h32.argtypes = [i32, P, P]
@@ -195,6 +200,23 @@ def gemm_acc(A: np.ndarray, B: np.ndarray, C: np.ndarray, op_a: str = "N", op_b:
                             _ptr(C), n, m * n, _ptr(out["c64"]), _ptr(out["n64"]),
                             _ptr(out["c32"]), _ptr(out["cm"]), n, m * n)
     return {key: v for key, v in out.items() if v is not None}
+
+
+def scan(X: np.ndarray, want=("c64", "n64", "c32", "cm")):
+    """Oracle quantities of the inclusive scan of every row of X
+    ([rows, len] or [..., len]): c64 running FP64 sums, n64 running sums of
+    |x|, c32 running FP32 sums, cm running sums of the split values."""
+    X = _f32(X)
+    shape = X.shape
+    X2 = X.reshape(-1, shape[-1]) if X.ndim != 2 else X
+    rows, length = X2.shape
+    out = {}
+    for key, dt in (("c64", np.float64), ("n64", np.float64),
+                    ("c32", np.float32), ("cm", np.float64)):
+        out[key] = np.zeros((rows, length), dtype=dt) if key in want else None
+    _load().oracle_scan(rows, length, _ptr(X2), length, _ptr(out["c64"]), _ptr(out["n64"]),
+                        _ptr(out["c32"]), _ptr(out["cm"]), length)
+    return {key: v.reshape(shape) for key, v in out.items() if v is not None}
 
 
 def dots(arows: np.ndarray, bcols: np.ndarray, want=("c64", "n64", "c32", "cm")):

@@ -25,6 +25,9 @@
  *     (Sec. 4.4, eq. corr-5).
  *   - oracle_gemm_acc: the accumulate form D = A*B + C0 of a fragment API
  *     (Sec. 2.2, Sec. 4.4), the same quantities with C0 as every sum's start.
+ *   - oracle_scan: inclusive prefix sums of each row, the product a^T U with
+ *     the upper-triangular all-ones U of Sec. 4.2 (eq. scan-mat, rule
+ *     u-rule), written as running sums.
  *   - oracle_householder: H = I - 2 u u^T built explicitly and applied to
  *     B (Sec. 4.2.1, eq. householder, read as an outer product).
  *   - oracle_givens: the rotation G(i, j, theta) of Sec. 4.3.1 (identity
@@ -436,6 +439,46 @@ void oracle_givens(int n, int gi, int gj, int ncols, int nitems, const int64_t *
                 if (CM)
                     CM[o] = sm;
             }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Scan: y_j = sum_{i <= j} x_i per row (Sec. 4.2, eq. scan-mat)           */
+/* ---------------------------------------------------------------------- */
+
+/* Row r of X (len values, row stride ldx) gives row r of each output (row
+ * stride ldy):
+ *   Y64 = running FP64 sum, N64 = running sum of |x|, Y32 = running FP32
+ *   sum (one rounded addition per element, left to right), YM = running
+ *   FP64 sum of the split values hi + lo 2^-11 (the method model of x . U:
+ *   every entry of U is 1 or 0, whose lo parts are 0). */
+void oracle_scan(int64_t rows, int len, const float *X, int64_t ldx,
+                 double *Y64, double *N64, float *Y32, double *YM, int64_t ldy)
+{
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t r = 0; r < rows; ++r) {
+        const float *x = X + r * ldx;
+        double s64 = 0.0, nrm = 0.0, sm = 0.0;
+        float s32 = 0.0f;
+        for (int j = 0; j < len; ++j) {
+            float v = x[j];
+            s64 += (double)v;
+            nrm += fabs((double)v);
+            s32 = s32 + v;
+            uint16_t h = oracle_f32_to_f16(v);
+            double vh = oracle_f16_to_f32(h);
+            double vl = oracle_f16_to_f32(oracle_f32_to_f16((v - (float)vh) * 2048.0f));
+            sm += vh + vl / 2048.0;
+            int64_t o = r * ldy + j;
+            if (Y64)
+                Y64[o] = s64;
+            if (N64)
+                N64[o] = nrm;
+            if (Y32)
+                Y32[o] = s32;
+            if (YM)
+                YM[o] = sm;
         }
     }
 }
