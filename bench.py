@@ -49,6 +49,7 @@ PEAK_FP16_MFMA_TFLOPS = 2516.6   # dense
 PEAK_FP32_VECTOR_TFLOPS = 157.3
 
 METRIC = "emulated-SGEMM TFLOP/s (batched)"
+SCAN_METRIC = "inclusive scan of FP32 rows, elements/s (batched)"
 
 # HBM traffic measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE), per
 # workload, with the hash of the kernel sources it was taken on
@@ -63,6 +64,7 @@ KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are ad
     "givens64_kernel": "rulebuilt.hip",
     "givens64_lds_kernel": "rulebuilt.hip",
     "gemm_acc_kernel": "gemm_acc.hip",
+    "scan_kernel": "scan.hip",
 }
 
 
@@ -166,6 +168,13 @@ def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO):
         def call():
             pkg.givens_emu_batched(i, j, c, s, B, C, mode=givens_mode)
         return call, C
+    if w.kind == "scan":
+        (X,) = inputs
+        Y = torch.empty_like(X)
+
+        def call():
+            pkg.sgemm_emu_scan(X, Y)
+        return call, Y
     if w.kind == "gemm_acc":
         At, B, Cin = inputs
         D = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
@@ -207,6 +216,14 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
 
         def ref(items):
             return oracle.givens(i, j, cn, sn, Bn, items=items, want=("c64", "n64", "c32"))
+    elif w.kind == "scan":
+        (X,) = host_inputs
+
+        def run(items):
+            return oracle.scan(X[items].numpy(), want=("c32",))
+
+        def ref(items):
+            return oracle.scan(X[items].numpy(), want=("c64", "n64", "c32"))
     elif w.kind == "gemm_acc":
         At, B, Cin = host_inputs
 
@@ -235,7 +252,8 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
         def ref(items):
             return oracle.gemm(A[items].numpy(), B[items].numpy(), want=("c64", "n64", "c32"))
 
-    per_item = 2.0 * w.m * w.n * w.k
+    per_item = w.flops / w.batch
+    scale, unit = (1e9, "Gelem/s") if w.kind == "scan" else (1e12, "TFLOP/s")
     if w.batch == 1:
         # one huge product: sample whole output rows instead of items
         A, B = host_inputs
@@ -285,7 +303,7 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
            "max_rel_err_fp32": oracle.max_rel_err(r["c32"], r["c64"], r["n64"]),
            "sample": f"items 0..{len(acc_items) - 1}"}
     sample = f"{n} of {w.batch} batch items" + (f", {reps} passes" if reps > 1 else "")
-    return {"value": per_item * n * reps / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
+    return {"value": per_item * n * reps / dt / scale, "unit": unit, "cores": threads,
             "kind": "oracle", "sample": sample, "seconds": dt}, acc
 
 
@@ -346,13 +364,18 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
 
     flops = w.flops
     tflops = flops / (ms_step * 1e-3) / 1e12
+    metric, value, unit = METRIC, tflops, "TFLOP/s"
+    if w.kind == "scan":
+        # one addition per element; the matrix form's MFMA work (12 MFMAs
+        # of 32x32x16 per 2048 elements) is far below the HBM floor
+        metric, value, unit = SCAN_METRIC, flops / (ms_step * 1e-3) / 1e9, "Gelem/s"
     # dominant (and only) kernel: one launch per step.  The bound is the
     # roof with the longer floor: HBM bytes at 8 TB/s or fp16 MFMA flops (3
     # per emulated flop) at the dense peak.
     bytes_alg = w.algorithmic_bytes
     t_hbm = bytes_alg / (PEAK_HBM_GBS * 1e9)
     t_mfma = 3 * flops / (PEAK_FP16_MFMA_TFLOPS * 1e12)
-    if t_mfma > t_hbm:
+    if t_mfma > t_hbm and w.kind != "scan":
         roof = {"bound": "mfma", "achieved": 3 * flops / (ms_step * 1e-3) / 1e12,
                 "peak": PEAK_FP16_MFMA_TFLOPS, "unit": "TFLOP/s"}
     else:
@@ -364,6 +387,8 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         kernel = "givens64_lds_kernel" if givens_mode == pkg.GIVENS_LDS else "givens64_kernel"
     elif w.kind == "gemm_acc":
         kernel = "gemm_acc_kernel"
+    elif w.kind == "scan":
+        kernel = "scan_kernel"
     elif w.kind == "gemm":
         A, B = dev_inputs
         resolved, kernel = pkg.sgemm_emu_resolve_policy(A, B, C, policy=policy)
@@ -376,9 +401,9 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     roof["traffic"] = measured_traffic(tkey, roof["kernel"])
 
     out = {
-        "metric": METRIC,
-        "value": tflops,
-        "unit": "TFLOP/s",
+        "metric": metric,
+        "value": value,
+        "unit": unit,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,

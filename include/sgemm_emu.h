@@ -269,6 +269,23 @@ int givens_emu_batched(int n, int i, int j,
                        int batch, int mode, hipStream_t stream);
 
 /*
+ * Batched inclusive scan through a rule-built matrix (Sec. 4.2, eq.
+ * scan-mat): for every row r in [0, rows),
+ *   Y[r][j] := sum_{i <= j} X[r][i],   j in [0, len)
+ * computed as the product of the row with the upper-triangular all-ones
+ * matrix U (u_ij = 1 for i <= j), whose operand fragments are generated from
+ * that rule with foreach_ij, in emulated FP32 (Sec. 4.4) on 64-column chunks
+ * chained by an FP32 running total.  X: rows x len, row stride ldx >=
+ * max(1, len); Y likewise with ldy.  Y may be X itself (ldy == ldx) for an
+ * in-place scan; any other overlap is an error.  Rows are independent; a
+ * wavefront scans 32 rows, so parallelism comes from the number of rows.
+ * Supported: rows < 2^30 (else SGEMM_EMU_ERR_UNSUPPORTED).
+ * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL, _ALIAS, _UNSUPPORTED, _HIP.
+ */
+int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx,
+                   float* Y, int64_t ldy, hipStream_t stream);
+
+/*
  * The split of Sec. 4.4 (eqs. corr-1/corr-2) applied elementwise on the
  * device: hi[i], lo[i] receive the binary16 bit patterns of
  * toFP16(x[i]) and toFP16((x[i] - toFP32(hi)) * 2^11).  count >= 0; x, hi

@@ -19,7 +19,7 @@ import os
 __all__ = [
     "SgemmEmuError", "lib_path", "load",
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
-    "sgemm_emu_batched_acc",
+    "sgemm_emu_batched_acc", "sgemm_emu_scan",
     "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
     "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
     "sgemm_emu_last_hip_error",
@@ -45,7 +45,7 @@ ROW_MAJOR, COL_MAJOR = 0, 1
 # Every symbol declared in include/sgemm_emu.h.
 EXPORTED_SYMBOLS = (
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
-    "sgemm_emu_batched_acc",
+    "sgemm_emu_batched_acc", "sgemm_emu_scan",
     "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
     "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
     "sgemm_emu_last_hip_error",
@@ -107,6 +107,7 @@ def load():
                                       ctypes.POINTER(ctypes.c_char_p)], i32),
         "sgemm_emu_batched_acc": ([i32, i32, i32, i32, i32, i32, P, i32, P, i32, P, i32, P, i32,
                                    i32, Stride4, i32, i32, P], i32),
+        "sgemm_emu_scan": ([i64, i32, P, i64, P, i64, P], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
         "givens_emu_batched": ([i32, i32, i32, P, P, i64, P, i32, i64, i32, P, i32, i64, i32,
                                 i32, P], i32),
@@ -281,6 +282,44 @@ def sgemm_emu_batched_acc(A, B, C=None, D=None, *, op_a: int = OP_N, op_b: int =
                                       int(shape), int(ec), _stream(stream))
     _check(rc, "sgemm_emu_batched_acc")
     return D
+
+
+def sgemm_emu_scan(X, Y=None, *, stream=None):
+    """Inclusive scan of every row: Y[..., j] = sum_{i <= j} X[..., i].
+
+    X: float32 device tensor whose last dimension is the row and whose rows
+    are evenly spaced (2-D with contiguous rows, or any contiguous tensor).
+    Y: same shape (allocated if None); Y may be X (in place)."""
+    import torch
+
+    if X.dtype != torch.float32 or not X.is_cuda:
+        raise ValueError("X must be a float32 device tensor")
+    if X.dim() == 2:
+        rows, length = X.shape
+        if length > 1 and X.stride(1) != 1:
+            raise ValueError("X rows must be contiguous")
+        ldx = X.stride(0) if rows > 1 else max(length, 1)
+    else:
+        if not X.is_contiguous():
+            raise ValueError("X must be contiguous (or 2-D with contiguous rows)")
+        length = X.shape[-1] if X.dim() else 1
+        rows = X.numel() // max(length, 1)
+        ldx = max(length, 1)
+    if Y is None:
+        Y = torch.empty(X.shape, dtype=torch.float32, device=X.device)
+    if Y.shape != X.shape or Y.dtype != torch.float32 or not Y.is_cuda:
+        raise ValueError("Y must be a float32 device tensor of X's shape")
+    if Y.dim() == 2:
+        if length > 1 and Y.stride(1) != 1:
+            raise ValueError("Y rows must be contiguous")
+        ldy = Y.stride(0) if rows > 1 else max(length, 1)
+    else:
+        if not Y.is_contiguous():
+            raise ValueError("Y must be contiguous (or 2-D with contiguous rows)")
+        ldy = max(length, 1)
+    rc = load().sgemm_emu_scan(rows, length, _ptr(X), ldx, _ptr(Y), ldy, _stream(stream))
+    _check(rc, "sgemm_emu_scan")
+    return Y
 
 
 def householder_emu_batched(u, B, C=None, *, stream=None):

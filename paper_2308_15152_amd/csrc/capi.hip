@@ -382,6 +382,30 @@ int givens_emu_batched(int n, int i, int j, const float* c, const float* s, int6
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
+int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx, float* Y, int64_t ldy,
+                   hipStream_t stream) {
+    if (rows < 0 || len < 0) return SGEMM_EMU_ERR_DIM;
+    if (ldx < (len > 1 ? len : 1) || ldy < (len > 1 ? len : 1)) return SGEMM_EMU_ERR_LD;
+    if (rows == 0 || len == 0) return SGEMM_EMU_OK;
+    // one wave per 32 rows, 4 waves per workgroup, below 2^31 work-items
+    if ((rows + 127) / 128 >= (int64_t(1) << 31) / 256) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (X == nullptr || Y == nullptr) return SGEMM_EMU_ERR_NULL;
+    const Extent ex = extent(X, 1, rows, len, ldx, 0);
+    const Extent ey = extent(Y, 1, rows, len, ldy, 0);
+    const bool in_place = X == Y && ldx == ldy;
+    if (!in_place && overlap(ex, ey)) return SGEMM_EMU_ERR_ALIAS;
+    sgemm_emu::ScanArgs a;
+    a.rows = rows;
+    a.len = len;
+    a.X = X;
+    a.ldx = ldx;
+    a.Y = Y;
+    a.ldy = ldy;
+    a.vec = ((uintptr_t)X % 16 == 0) && ldx % 4 == 0;
+    hipError_t e = sgemm_emu::launch_scan(a, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
 int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                     hipStream_t stream) {
     if (count < 0) return SGEMM_EMU_ERR_DIM;

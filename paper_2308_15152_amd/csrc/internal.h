@@ -87,6 +87,19 @@ struct AccArgs {
 // shape: 0 = 16x16x32, 1 = 32x32x16.
 hipError_t launch_gemm_acc(const AccArgs& a, int shape, bool ec, hipStream_t stream);
 
+// Inclusive scan of each row of X (rows x len, row stride ldx) into Y.
+struct ScanArgs {
+    int64_t rows;
+    int len;
+    const float* X;
+    int64_t ldx;
+    float* Y;
+    int64_t ldy;
+    bool vec;  // X 16-byte aligned with ldx a multiple of 4
+};
+
+hipError_t launch_scan(const ScanArgs& a, hipStream_t stream);
+
 hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                         hipStream_t stream);
 

@@ -22,6 +22,8 @@ Workloads (row-major, contiguous, FP32):
   entries uniform(-1, 1),                                                  seed 6
 * ``gemm_acc_128``  batch 4096, D = A^T B + C with A stored k x m (128 x 128),
   B 128 x 128, C 128 x 128, entries uniform(-1, 1), drawn A, B, C,         seed 8
+* ``scan_2048``  131072 rows of 2048 values uniform(-1, 1) (batch = rows,
+  n = the row length), inclusive scan of every row,                        seed 9
 * ``givens_64``  batch 262144, rotation plane (i, j) = (5, 37) of n = 64,
   theta uniform in [0, 2 pi) per item with c, s = cos, sin theta evaluated
   in FP64 and rounded to FP32, B 64 x 64 uniform(-1, 1),                   seed 7
@@ -39,7 +41,7 @@ import torch
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str        # "gemm", "gemm_acc", "householder" or "givens"
+    kind: str        # "gemm", "gemm_acc", "householder", "givens" or "scan"
     batch: int
     m: int
     n: int
@@ -53,7 +55,9 @@ class Workload:
         """Emulated flops counted as 2 m n k per item (Sec. 4.4.2); for the
         Householder and Givens workloads the left matrix is formed
         explicitly as a fragment, so the same dense count applies with
-        m = k = 64."""
+        m = k = 64.  A scan counts one addition per element."""
+        if self.kind == "scan":
+            return float(self.batch * self.n)
         return 2.0 * self.m * self.n * self.k * self.batch
 
     @property
@@ -64,6 +68,8 @@ class Workload:
             per = 4 * (self.m + self.k * self.n + self.m * self.n)
         elif self.kind == "givens":
             per = 4 * (2 + self.k * self.n + self.m * self.n)
+        elif self.kind == "scan":
+            per = 8 * self.n  # read the row, write its scan
         elif self.kind == "gemm_acc":
             # read A, B and C, write D
             per = 4 * (self.m * self.k + self.k * self.n + 2 * self.m * self.n)
@@ -90,6 +96,7 @@ for _k in PAPER_SWEEP_K:
                                          "uniform", 6)
 
 
+WORKLOADS["scan_2048"] = Workload("scan_2048", "scan", 131072, 1, 2048, 1, "uniform", 9)
 WORKLOADS["gemm_acc_128"] = Workload("gemm_acc_128", "gemm_acc", 4096, 128, 128, 128, "uniform", 8)
 WORKLOADS["givens_64"] = Workload("givens_64", "givens", 262144, 64, 64, 64, "givens", 7,
                                   (5, 37))
@@ -167,6 +174,8 @@ def workload_inputs(w: Workload, batch: int | None = None):
         return givens_inputs(b, w.m, w.n, w.seed)
     if w.kind == "gemm_acc":
         return gemm_acc_inputs(b, w.m, w.n, w.k, w.seed)
+    if w.kind == "scan":
+        return (uniform((b, w.n), _gen(w.seed)),)
     return gemm_inputs(b, w.m, w.n, w.k, w.seed, w.dist)
 
 

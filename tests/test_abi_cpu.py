@@ -298,6 +298,26 @@ def test_batched_acc_validation():
     assert acc(st=ok, C=PD, D=PD, ldc=64, ldd=48) == -5
 
 
+def test_scan_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+
+    def sc(rows=100, length=200, X=PA, ldx=200, Y=PB, ldy=200):
+        return lib.sgemm_emu_scan(rows, length, P(X), ldx, P(Y), ldy, P(0))
+
+    assert sc(rows=-1) == -1
+    assert sc(length=-1) == -1
+    assert sc(ldx=199) == -2
+    assert sc(ldy=0) == -2
+    assert sc(rows=0) == 0
+    assert sc(length=0) == 0
+    assert sc(rows=1 << 30) == -6
+    assert sc(X=0) == -3
+    assert sc(Y=0) == -3
+    assert sc(Y=PA + 4) == -5
+    assert sc(Y=PA, ldy=256, ldx=200) == -5
+
+
 def test_split_validation():
     lib = pkg.load()
     P = ctypes.c_void_p

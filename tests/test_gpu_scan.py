@@ -1,0 +1,87 @@
+"""Parity of the batched inclusive scan computed as x^T U with the
+upper-triangular all-ones U built from its rule by foreach_ij (Sec. 4.2,
+eq. scan-mat), in emulated FP32 (Sec. 4.4), against the scan oracle.
+
+* row counts around the 32-row wave (1, 31, 32, 33, 100) and lengths
+  around the 64-column chunk (1, 63, 64, 65, 200, 1000);
+* integer inputs give the exact running sums; a unit impulse gives a step;
+* in place, padded row strides, unaligned bases (the element-wise path);
+* the full-size workload on sampled rows.
+
+Tolerance: within a chunk an output is a sum of at most 64 split values
+accumulated by the matrix instruction, then one fused combine of the two
+accumulators and one addition of the carry; across chunks the carry adds
+one more rounding per chunk.  So with k = min(len, 64) + 2 ceil(len / 64)
+the element-wise bounds of the GEMM tests apply (gpu_util.gate):
+|Y - YM| <= (k + 2) 2^-23 N and |Y - Y64| <= (k + 8) 2^-23 N, N the running
+sum of |x|.  The ratio gate against the plain FP32 running sum is not
+applied: on short prefixes that sum is exact by construction.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2308_15152_amd as pkg
+import synth
+from gpu_util import device, gate, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _k_eff(length):
+    return min(length, 64) + 2 * ((length + 63) // 64)
+
+
+@pytest.mark.parametrize("rows", [1, 31, 32, 33, 100])
+@pytest.mark.parametrize("length", [1, 63, 64, 65, 200, 1000])
+def test_parity_shapes(rows, length):
+    print(f"case scan rows={rows} len={length}", flush=True)
+    X = synth.uniform((rows, length), synth.rng(rows * 7 + length))
+    Y = to_np(pkg.sgemm_emu_scan(X.to(device())))
+    ref = oracle.scan(X.numpy())
+    gate(Y, ref, _k_eff(length), f"scan {rows}x{length}", max_gate=False)
+
+
+def test_integer_exact_and_in_place():
+    X = synth.integer_matrix((70, 3000), synth.rng(5), -1000, 1000)
+    Xd = X.to(device())
+    pkg.sgemm_emu_scan(Xd, Xd)
+    exact = np.cumsum(X.numpy().astype(np.int64), axis=1)
+    assert np.array_equal(to_np(Xd), exact.astype(np.float32))
+
+
+def test_impulse_gives_step():
+    X = torch.zeros((40, 300))
+    X[3, 0] = 2.5
+    X[39, 299] = -1.0
+    X[17, 64] = 3.0
+    Y = to_np(pkg.sgemm_emu_scan(X.to(device())))
+    expect = np.cumsum(X.numpy().astype(np.float64), axis=1).astype(np.float32)
+    assert np.array_equal(Y, expect)
+
+
+@pytest.mark.parametrize("offset", [0, 1])
+def test_padded_and_unaligned(offset):
+    dev = device()
+    X = synth.uniform((45, 130), synth.rng(6))
+    buf = torch.zeros(45 * 136 + offset, device=dev)
+    Xv = buf[offset:].view(45, 136)[:, :130]
+    Xv.copy_(X.to(dev))
+    Ybuf = torch.full((45, 140), 5.0, device=dev)
+    pkg.sgemm_emu_scan(Xv, Ybuf[:, :130])
+    out = to_np(Ybuf)
+    gate(out[:, :130], oracle.scan(X.numpy()), _k_eff(130), "scan padded", max_gate=False)
+    assert np.all(out[:, 130:] == 5.0)
+
+
+def test_workload_scan_sampled():
+    w = synth.WORKLOADS["scan_2048"]
+    print(f"case workload=scan_2048 rows={w.batch} len={w.n}", flush=True)
+    (X,) = synth.workload_inputs(w)
+    Y = pkg.sgemm_emu_scan(X.to(device()))
+    rows = [0, 1, 31, 32, 4095, 65536, w.batch - 1]
+    Ys = to_np(Y[rows])
+    ref = oracle.scan(X[rows].numpy())
+    e = gate(Ys, ref, _k_eff(w.n), "scan_2048", max_gate=False)
+    print(f"scan_2048: err {e[0]:.3e} fp32 running sum {e[1]:.3e}")
