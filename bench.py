@@ -59,6 +59,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are added
     "bgemm_reg_kernel": "bgemm_reg.hip",
     "bgemm_big_kernel": "bgemm_big.hip",
+    "bgemm_big_stream_kernel": "bgemm_big.hip",
     "bgemm_emu_kernel": "bgemm.hip",
     "householder64_kernel": "rulebuilt.hip",
     "givens64_kernel": "rulebuilt.hip",
@@ -280,11 +281,17 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
         return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
                 "kind": "oracle", "sample": sample, "seconds": dt}, acc
 
-    n = 1
-    t0 = time.perf_counter()
-    run([0])
-    dt1 = time.perf_counter() - t0
-    n = int(min(w.batch, max(threads, target_s / max(dt1, 1e-4))))
+    # calibrate at full parallelism (at least one item per thread), growing
+    # the sample until it takes an eighth of the target
+    n = min(w.batch, threads)
+    while True:
+        t0 = time.perf_counter()
+        run(list(range(n)))
+        dt = time.perf_counter() - t0
+        if dt >= target_s / 8 or n >= w.batch:
+            break
+        n = min(w.batch, n * 4)
+    n = int(min(w.batch, max(n, n * target_s / max(dt, 1e-6))))
     items = list(range(n))
     # when the whole batch takes less than the target, time whole passes
     # until the target is reached

@@ -1,6 +1,6 @@
 // mfmae/wmma_tcec.hpp -- FP32 matrix-multiply-accumulate fragments with the
 // interface of a fragment API (fragment / fill_fragment / load_matrix_sync /
-// mma_sync / store_matrix_sync, Sec. 2.2), computed by the single-precision
+// mma_sync / store_matrix_sync, Sec. 2.3.1), computed by the single-precision
 // emulation of Sec. 4.4 on the gfx950 fp16 MFMA instructions.
 //
 // Code written for fp16 fragments switches to emulated FP32 by changing the

@@ -168,7 +168,7 @@ int sgemm_emu_resolve_policy(int m, int n, int k,
 /*
  * Batched multiply-accumulate in emulated FP32 with transposable operands:
  *   for t in [0, batch):  D_t := op(A_t) . op(B_t) + C_t
- * the matrix-multiply-accumulate of a fragment API (Sec. 2.2) computed by
+ * the matrix-multiply-accumulate of a fragment API (Sec. 2.3.1) computed by
  * the method of Sec. 4.4 through the library's fragment interface
  * (mfmae/wmma_tcec.hpp; the kernel is written with its load_matrix_sync,
  * mma_sync and store_matrix_sync).  op(A) is m x k, op(B) is k x n.
@@ -269,7 +269,7 @@ int givens_emu_batched(int n, int i, int j,
                        int batch, int mode, hipStream_t stream);
 
 /*
- * Batched inclusive scan through a rule-built matrix (Sec. 4.2, eq.
+ * Batched inclusive scan through a rule-built matrix (Sec. 4.1, eq.
  * scan-mat): for every row r in [0, rows),
  *   Y[r][j] := sum_{i <= j} X[r][i],   j in [0, len)
  * computed as the product of the row with the upper-triangular all-ones

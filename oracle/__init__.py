@@ -20,10 +20,10 @@ it follows:
   fmaf chain, ascending k) and the method-exact model of eq. corr-5 summed in
   FP64.
 * :func:`gemm_acc` -- D = op(A).op(B) + C (op: as stored or transposed),
-  the multiply-accumulate form of a fragment API (Sec. 2.2, Sec. 4.4): the
+  the multiply-accumulate form of a fragment API (Sec. 2.3.1, Sec. 4.4): the
   same four quantities with C as the first term of every sum.
 * :func:`scan` -- inclusive prefix sums of each row: a^T U with U the
-  upper-triangular all-ones matrix of Sec. 4.2 (eq. scan-mat), written as
+  upper-triangular all-ones matrix of Sec. 4.1 (eq. scan-mat), written as
   running sums (FP64, |x|, FP32, and the split model).
 * :func:`householder` -- H = I - 2 u u^T formed explicitly and applied to B
   (Sec. 4.2.1, eq. householder, read as an outer product of u).

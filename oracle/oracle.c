@@ -24,9 +24,9 @@
  *     A_F16 B_F16 + (dA_F16 B_F16 + A_F16 dB_F16) / 2^11 summed in FP64
  *     (Sec. 4.4, eq. corr-5).
  *   - oracle_gemm_acc: the accumulate form D = A*B + C0 of a fragment API
- *     (Sec. 2.2, Sec. 4.4), the same quantities with C0 as every sum's start.
+ *     (Sec. 2.3.1, Sec. 4.4), the same quantities with C0 as every sum's start.
  *   - oracle_scan: inclusive prefix sums of each row, the product a^T U with
- *     the upper-triangular all-ones U of Sec. 4.2 (eq. scan-mat, rule
+ *     the upper-triangular all-ones U of Sec. 4.1 (eq. scan-mat, rule
  *     u-rule), written as running sums.
  *   - oracle_householder: H = I - 2 u u^T built explicitly and applied to
  *     B (Sec. 4.2.1, eq. householder, read as an outer product).
@@ -219,7 +219,7 @@ void oracle_gemm(int batch, int m, int n, int k,
 }
 
 /* Accumulate form D = A * B + C0 (the matrix-multiply-accumulate of a
- * fragment API, Sec. 2.2 and Sec. 4.4): the same four quantities as
+ * fragment API, Sec. 2.3.1 and Sec. 4.4): the same four quantities as
  * oracle_gemm with C0 as the starting value of every sum,
  *   C64 = C0 + sum_k A B          (FP64, C0 first, then k ascending)
  *   N64 = |C0| + sum_k |A| |B|
@@ -444,7 +444,7 @@ void oracle_givens(int n, int gi, int gj, int ncols, int nitems, const int64_t *
 }
 
 /* ---------------------------------------------------------------------- */
-/* Scan: y_j = sum_{i <= j} x_i per row (Sec. 4.2, eq. scan-mat)           */
+/* Scan: y_j = sum_{i <= j} x_i per row (Sec. 4.1, eq. scan-mat)           */
 /* ---------------------------------------------------------------------- */
 
 /* Row r of X (len values, row stride ldx) gives row r of each output (row

@@ -735,6 +735,13 @@ bool big_supported(const GemmArgs& a, int tile, int flow) {
     }
 }
 
+// 256x128 runs one workgroup per CU: with few k chunks per tile, the
+// persistent stream hides the per-tile pipeline fill (measured 1.14x on
+// 1024 x 256^3); long k loops amortize it themselves.
+bool big_streams(const GemmArgs& a, int tile, int flow) {
+    return flow == SGEMM_EMU_FLOW_SPLIT && tile == SGEMM_EMU_TILE_256x128 && a.k <= 2048;
+}
+
 hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream) {
     if (!big_supported(a, tile, flow)) return hipErrorInvalidValue;
     if (flow == SGEMM_EMU_FLOW_DIRECT) return launch_big_cfg<Big128x128Direct>(a, stream);
@@ -742,11 +749,8 @@ hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t st
     switch (tile) {
         case SGEMM_EMU_TILE_128x128: return launch_big_cfg<Big128x128>(a, stream);
         case SGEMM_EMU_TILE_256x128:
-            // one workgroup per CU: with few k chunks per tile, the
-            // persistent stream hides the per-tile pipeline fill (measured
-            // 1.14x on 1024 x 256^3); long k loops amortize it themselves
-            return a.k <= 2048 ? launch_big_stream_cfg<Big256x128>(a, stream)
-                               : launch_big_cfg<Big256x128>(a, stream);
+            return big_streams(a, tile, flow) ? launch_big_stream_cfg<Big256x128>(a, stream)
+                                              : launch_big_cfg<Big256x128>(a, stream);
         default: return launch_big_cfg<Big128x256>(a, stream);
     }
 }

@@ -240,7 +240,10 @@ int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const
                           pol.tile, a, kern);
     if (rc != SGEMM_EMU_OK) return rc;
     *out = pol;
-    if (kernel) *kernel = kernel_name(kern);
+    if (kernel)
+        *kernel = kern == K_BIG && sgemm_emu::big_streams(a, pol.tile, pol.flow)
+                      ? "bgemm_big_stream_kernel"
+                      : kernel_name(kern);
     return SGEMM_EMU_OK;
 }
 

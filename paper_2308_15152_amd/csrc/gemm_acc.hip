@@ -1,6 +1,6 @@
 // Batched D = op(A) . op(B) + C in emulated FP32, written entirely with the
 // fragment interface of mfmae/wmma_tcec.hpp: the multiply-accumulate form of
-// a fragment API (Sec. 2.2) with the error-correcting emulation of Sec. 4.4
+// a fragment API (Sec. 2.3.1) with the error-correcting emulation of Sec. 4.4
 // behind the same calls (load_matrix_sync, mma_sync, store_matrix_sync).
 //
 // Each wavefront owns a 2 x 2 block of fragments (64 x 64 outputs with the

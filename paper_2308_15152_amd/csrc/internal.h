@@ -36,6 +36,8 @@ hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t str
 // alignment allow the tile.
 bool big_supported(const GemmArgs& a, int tile, int flow);
 hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream);
+// True if launch_gemm_big runs the persistent stream form of the kernel.
+bool big_streams(const GemmArgs& a, int tile, int flow);
 
 struct HouseholderArgs {
     int ncols;

@@ -1,5 +1,5 @@
 // Batched inclusive scan y_j = sum_{i <= j} x_i of every row, as the product
-// x^T U with the upper-triangular all-ones U (Sec. 4.2, eq. scan-mat, rule
+// x^T U with the upper-triangular all-ones U (Sec. 4.1, eq. scan-mat, rule
 // u-rule), in emulated FP32 (Sec. 4.4).
 //
 // One wavefront scans 32 rows, 64 columns (a chunk) at a time.  The chunk is

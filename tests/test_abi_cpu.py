@@ -136,6 +136,10 @@ def test_resolve_policy():
     s256 = 256 * 256
     assert _resolve(256, 256, 256, 1024, (s256, s256, s256)) == (0, (pkg.FLOW_SPLIT, 1,
                                                                      pkg.TILE_256x128))
+    # 256 x 128 tiles with k <= 2048 run the persistent stream form
+    assert _resolve.kernel == "bgemm_big_stream_kernel"
+    assert _resolve(256, 256, 4096, 4, (256 * 4096, 4096 * 256, s256)) == (
+        0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
     assert _resolve.kernel == "bgemm_big_kernel"
     assert _resolve(8192, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
     assert _resolve.kernel == "bgemm_big_kernel"

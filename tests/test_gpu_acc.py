@@ -1,6 +1,6 @@
 """Parity of D = op(A).op(B) + C computed by the kernel written with the
 fragment interface (mfmae/wmma_tcec.hpp: load_matrix_sync, mma_sync,
-store_matrix_sync; Sec. 2.2 and Sec. 4.4), against the accumulate-form
+store_matrix_sync; Sec. 2.3.1 and Sec. 4.4), against the accumulate-form
 oracle:
 
 * every combination of instruction shape, operand transposes and C/D

@@ -149,7 +149,7 @@ def test_full_tile_kernel_shapes(flow, tile, shape):
     Ad, Bd = Ab[:, :, :k], Bb[:, :, :n]
     Cd = torch.empty((batch, m, n), device=dev)
     _, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, Cd, policy=policy)
-    assert kern == "bgemm_big_kernel"
+    assert kern in ("bgemm_big_kernel", "bgemm_big_stream_kernel")
     pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=policy)
     ref = oracle.gemm(A.numpy(), B.numpy())
     gate(to_np(Cd), ref, k, f"full-tile {tile} {shape}")

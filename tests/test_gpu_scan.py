@@ -1,5 +1,5 @@
 """Parity of the batched inclusive scan computed as x^T U with the
-upper-triangular all-ones U built from its rule by foreach_ij (Sec. 4.2,
+upper-triangular all-ones U built from its rule by foreach_ij (Sec. 4.1,
 eq. scan-mat), in emulated FP32 (Sec. 4.4), against the scan oracle.
 
 * row counts around the 32-row wave (1, 31, 32, 33, 100) and lengths

@@ -1,5 +1,5 @@
 """Pins of the accumulate-form oracle D = op(A).op(B) + C (the
-multiply-accumulate of a fragment API, Sec. 2.2; emulated as in Sec. 4.4):
+multiply-accumulate of a fragment API, Sec. 2.3.1; emulated as in Sec. 4.4):
 
 * C = 0 reduces it to the plain GEMM oracle, quantity for quantity;
 * A = 0 or k = 0 leaves D = C exactly, and N = |C|;

@@ -1,4 +1,4 @@
-"""Pins of the scan oracle (Sec. 4.2, eq. scan-mat: the inclusive scan of a
+"""Pins of the scan oracle (Sec. 4.1, eq. scan-mat: the inclusive scan of a
 row a is a^T U with u_ij = 1 for i <= j, else 0):
 
 * on short rows every quantity equals the GEMM oracle applied to the
