@@ -2,16 +2,23 @@
 // x^T U with the upper-triangular all-ones U (Sec. 4.1, eq. scan-mat, rule
 // u-rule), in emulated FP32 (Sec. 4.4).
 //
-// One wavefront scans 32 rows, 64 columns (a chunk) at a time.  The chunk is
-// the 32 x 64 A operand X (split into hi and lo in registers); U's 64 x 64
-// block is the B operand, built once per wave with foreach_ij from the rule
-// u_ij = [i <= j] and never stored: its 16 x 32 pieces for k step s and
-// column block cb are all-zero for cb = 0, s >= 2, so a chunk takes 6 piece
-// products.  U's entries are 0 and 1, whose lo parts are 0, so the
-// correction reduces to lo(X) U: two MFMAs per piece instead of three.
-// Chunks are chained by a carry: the running total of each row (column 63
-// of the previous chunk's result, broadcast from the lanes that hold it)
-// is added to every output of the row.  The next chunk's X is loaded while
+// A wavefront scans whole rows, 1024 values (a block) at a time.  The block
+// is read as a 32 x 32 matrix Z of 32 consecutive segments (Z[n][k] is value
+// 32 n + k of the block) and scanned in two levels:
+//   * within segments, as the transposed product S^T = U^T Z^T: U^T's
+//     32 x 32 block is the A operand, built once per wave with foreach_ij
+//     from the rule (element (i, k) of U^T is [k <= i]) and never stored; Z
+//     is the B operand (two 16-wide k steps, split into hi and lo in
+//     registers).  U's entries are 0 and 1, whose lo parts are 0, so the
+//     correction reduces to U^T lo(Z^T): four MFMAs per block;
+//   * across segments, an exclusive scan of the 32 segment totals over the
+//     lanes (five shuffle steps), plus the running total of the row's
+//     earlier blocks, added to every value of the segment.
+// Lane (n, g) = (l % 32, l / 32) holds values 32 n + 16 s + 8 g .. + 7 of the
+// block as its operand and, as its accumulator, outputs 32 n + 8 q + 4 g ..
+// + 3 for q = 0..3: every load and store is 16 bytes, and one wave's
+// instructions together cover a contiguous 4 KiB.  Over whole blocks of
+// 16-byte aligned rows the loads of the next kBuf blocks are in flight while
 // the current one is multiplied.
 #include "internal.h"
 #include "mfmae/frag.hpp"
@@ -27,130 +34,192 @@ using mfmae::Shape32;
 using mfmae::Use;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-using FragB = mfmae::fragment<Shape32, Use::B, _Float16>;
+using FragA = mfmae::fragment<Shape32, Use::A, _Float16>;
 
 constexpr int kWaves = 4;
 
-// The 8 values lane l holds of a 32-row, 16-column piece of X at k step s:
-// row r0 + l % 32, columns c0 + 16 s + 8 (l / 32) .. + 7.
-struct Chunk {
-    float x[4][8];
+constexpr int kBuf = 4;         // block buffers per wave
+constexpr int kRowsPerWave = 8;  // rows a wave scans, one after another
+
+// The 16 values lane (n, g) holds of a block as B operand: block values
+// 32 n + 16 s + 8 g + v, s = 0, 1, v = 0..7.
+struct Block {
+    float x[2][8];
 };
 
-__device__ inline void load_chunk(Chunk& ch, const ScanArgs& p, int64_t r0, int c0, bool fast) {
+// Whole block inside a 16-byte aligned row: four 16-byte loads.
+__device__ inline void load_fast(Block& b, const float* row, int c0) {
     const int l = threadIdx.x & 63;
-    const int64_t row = r0 + (l & 31);
-    const int col = c0 + 8 * (l >> 5);
-    if (fast) {
-        const float* q = p.X + row * p.ldx + col;
+    const float* q = row + c0 + 32 * (l & 31) + 8 * (l >> 5);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            const f32x4 v0 = *reinterpret_cast<const f32x4*>(q + 16 * s);
-            const f32x4 v1 = *reinterpret_cast<const f32x4*>(q + 16 * s + 4);
+    for (int s = 0; s < 2; ++s) {
+        const f32x4 v0 = *reinterpret_cast<const f32x4*>(q + 16 * s);
+        const f32x4 v1 = *reinterpret_cast<const f32x4*>(q + 16 * s + 4);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                ch.x[s][v] = v0[v];
-                ch.x[s][v + 4] = v1[v];
-            }
+        for (int v = 0; v < 4; ++v) {
+            b.x[s][v] = v0[v];
+            b.x[s][v + 4] = v1[v];
         }
-    } else {
-        const bool row_ok = row < p.rows;
-        const float* q = p.X + (row_ok ? row : 0) * p.ldx;
+    }
+}
+
+// Any block: element loads, zero past the row's end.
+__device__ inline void load_bounded(Block& b, const float* row, int c0, int len) {
+    const int l = threadIdx.x & 63;
+    const int base = c0 + 32 * (l & 31) + 8 * (l >> 5);
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-            for (int v = 0; v < 8; ++v) {
-                const int cc = col + 16 * s + v;
-                ch.x[s][v] = (row_ok && cc < p.len) ? q[cc] : 0.0f;
-            }
+        for (int v = 0; v < 8; ++v) {
+            const int cc = base + 16 * s + v;
+            b.x[s][v] = cc < len ? row[cc] : 0.0f;
+        }
+}
+
+// y = carry + scan of the block; carry becomes the row's running total
+// after it.  Accumulator element e of lane (n, g) is block value
+// 32 n + 8 (e / 4) + 4 g + e % 4.
+__device__ inline void scan_block(const Block& b, const half8_t (&Ut)[2], float& carry,
+                                  float (&y)[16]) {
+    const int l = threadIdx.x & 63;
+    const int n = l & 31;
+    f32x16_t acc, cor;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        acc[e] = 0.0f;
+        cor[e] = 0.0f;
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        half8_t xh, xl;
+        mfmae::tcec::split8(b.x[s], xh, xl);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ut[s], xh, acc, 0, 0, 0);
+        cor = __builtin_amdgcn_mfma_f32_32x32x16_f16(Ut[s], xl, cor, 0, 0, 0);
+    }
+    // scans within the segments
+    float z[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) z[e] = __builtin_fmaf(cor[e], mfmae::tcec::kLoScaleInv, acc[e]);
+    // segment totals: the last value of segment n is element 15 of lane
+    // 32 + n; inclusive scan of the totals over n (both half-waves hold it)
+    float incl = __shfl(z[15], 32 + n, 64);
+#pragma unroll
+    for (int d = 1; d < 32; d *= 2) {
+        const float u = __shfl_up(incl, d, 32);
+        if (n >= d) incl += u;
+    }
+    const float before = __shfl_up(incl, 1, 32);  // total of segments 0..n-1
+    const float offset = n == 0 ? carry : carry + before;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) y[e] = offset + z[e];
+    carry = carry + __shfl(incl, 31, 64);
+}
+
+__device__ inline void store_fast(float* row, int c0, const float (&y)[16]) {
+    const int l = threadIdx.x & 63;
+    float* q = row + c0 + 32 * (l & 31) + 4 * (l >> 5);
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<f32x4*>(q + 8 * g) = f32x4{y[4 * g], y[4 * g + 1], y[4 * g + 2],
+                                                     y[4 * g + 3]};
+}
+
+__device__ inline void store_bounded(float* row, int c0, int len, const float (&y)[16]) {
+    const int l = threadIdx.x & 63;
+    const int base = c0 + 32 * (l & 31) + 4 * (l >> 5);
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int col = base + 8 * (e >> 2) + (e & 3);
+        if (col < len) row[col] = y[e];
     }
 }
 
 __global__ __launch_bounds__(64 * kWaves, 2) void scan_kernel(ScanArgs p) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int l = threadIdx.x & 63;
-    const int64_t group = (int64_t)blockIdx.x * kWaves + wave;
-    const int64_t r0 = group * 32;
-    if (r0 >= p.rows) return;  // whole wave; no barrier below
-    const bool rows_full = r0 + 32 <= p.rows;
+    const int64_t r_first = ((int64_t)blockIdx.x * kWaves + wave) * kRowsPerWave;
+    if (r_first >= p.rows) return;  // whole wave; no barrier below
+    const int nrows = (int)min((int64_t)kRowsPerWave, p.rows - r_first);
 
-    // U pieces (k step s, column block cb): element (kk, j) is
-    // [16 s + kk <= 32 cb + j]; hi only (lo is 0 for 0 and 1).
-    half8_t U[4][2];
+    // U^T's diagonal block for k step s: element (i, kk) is [16 s + kk <= i];
+    // hi only (lo is 0 for 0 and 1).
+    half8_t Ut[2];
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-            mfmae::foreach_ij<FragB>([&](int e, int kk, int j) {
-                U[s][cb][e] = (16 * s + kk <= 32 * cb + j) ? (_Float16)1.0f : (_Float16)0.0f;
-            });
+    for (int s = 0; s < 2; ++s)
+        mfmae::foreach_ij<FragA>([&](int e, int i, int kk) {
+            Ut[s][e] = (16 * s + kk <= i) ? (_Float16)1.0f : (_Float16)0.0f;
+        });
 
-    float carry[16];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) carry[e] = 0.0f;
+    float carry = 0.0f;
+    float y[16];
 
-    auto fast_at = [&](int c0) { return p.vec && rows_full && c0 + 64 <= p.len; };
-    Chunk cur;
-    load_chunk(cur, p, r0, 0, fast_at(0));
-    for (int c0 = 0; c0 < p.len; c0 += 64) {
-        Chunk nxt;
-        const int c1 = c0 + 64;
-        if (c1 < p.len) load_chunk(nxt, p, r0, c1, fast_at(c1));
-
-        half8_t xh[4], xl[4];
+    if (p.vec && p.len % 1024 == 0) {
+        // Whole blocks of aligned rows, as one sequence f = (row, block) of
+        // nf blocks: kBuf block buffers in turn.  A step scans one buffer's
+        // block, stores it and reloads the buffer with block f + kBuf.  Loads
+        // are unconditional (past the end they re-read the last block) and
+        // the first round of steps is peeled, so the loop is entered with the
+        // same memory operations pending as on every later iteration and the
+        // wait before each block covers that block's loads only.
+        const int nb = p.len / 1024;
+        const int nf = nrows * nb;
+        const int last = nf - 1;
+        auto row_in = [&](int f) { return p.X + (r_first + f / nb) * p.ldx; };
+        auto row_out = [&](int f) { return p.Y + (r_first + f / nb) * p.ldy; };
+        auto load = [&](Block& b, int f) {
+            const int fc = min(f, last);
+            load_fast(b, row_in(fc), 1024 * (fc % nb));
+        };
+        // the scheduling barrier keeps each step's reload in place, so the
+        // blocks really are loaded kBuf steps ahead
+        auto step = [&](Block& b, int f) {
+            if (f % nb == 0) carry = 0.0f;
+            scan_block(b, Ut, carry, y);
+            store_fast(row_out(f), 1024 * (f % nb), y);
+            load(b, f + kBuf);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        Block buf[kBuf];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) mfmae::tcec::split8(cur.x[s], xh[s], xl[s]);
-        f32x16_t acc[2], cor[2];
+        for (int i = 0; i < kBuf; ++i) load(buf[i], i);
+        int f = 0;
+        if (nf >= kBuf) {
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+            for (int i = 0; i < kBuf; ++i) step(buf[i], i);
+            for (f = kBuf; f + kBuf <= nf; f += kBuf) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                acc[cb][e] = 0.0f;
-                cor[cb][e] = 0.0f;
-            }
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                if (cb == 0 && s >= 2) continue;  // that piece of U is zero
-                acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xh[s], U[s][cb], acc[cb], 0, 0, 0);
-                cor[cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xl[s], U[s][cb], cor[cb], 0, 0, 0);
-            }
-
-        // y = carry + (acc + cor 2^-11); element e of block cb is row
-        // 8 (e / 4) + 4 (l / 32) + e % 4, column c0 + 32 cb + l % 32
-        float y[2][16];
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                y[cb][e] = carry[e] +
-                           __builtin_fmaf(cor[cb][e], mfmae::tcec::kLoScaleInv, acc[cb][e]);
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            const int col = c0 + 32 * cb + (l & 31);
-            if (col < p.len) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int64_t row = r0 + mfmae::layout<Shape32, Use::Acc>::row(l, e);
-                    if (rows_full || row < p.rows) p.Y[row * p.ldy + col] = y[cb][e];
-                }
+                for (int i = 0; i < kBuf; ++i) step(buf[i], f + i);
             }
         }
-        // running totals: column 63 of this chunk, held by lane 31 + 32 (l / 32)
-        // for the same rows as this lane's elements
-        const int src = 31 + 32 * (l >> 5);
+        // buf[i] holds block f + i for the remaining blocks
 #pragma unroll
-        for (int e = 0; e < 16; ++e) carry[e] = __shfl(y[1][e], src, 64);
-        if (c1 < p.len) cur = nxt;
+        for (int i = 0; i < kBuf - 1; ++i) {
+            if (f + i < nf) {
+                if ((f + i) % nb == 0) carry = 0.0f;
+                scan_block(buf[i], Ut, carry, y);
+                store_fast(row_out(f + i), 1024 * ((f + i) % nb), y);
+            }
+        }
+        return;
+    }
+    // any length or alignment: element loads and stores, one block at a time
+    for (int r = 0; r < nrows; ++r) {
+        const float* xin = p.X + (r_first + r) * p.ldx;
+        float* yout = p.Y + (r_first + r) * p.ldy;
+        carry = 0.0f;
+        for (int c0 = 0; c0 < p.len; c0 += 1024) {
+            Block b;
+            load_bounded(b, xin, c0, p.len);
+            scan_block(b, Ut, carry, y);
+            store_bounded(yout, c0, p.len, y);
+        }
     }
 }
 
 }  // namespace
 
 hipError_t launch_scan(const ScanArgs& a, hipStream_t stream) {
-    const int64_t groups = (a.rows + 31) / 32;
-    const int64_t blocks = (groups + kWaves - 1) / kWaves;
+    const int64_t waves = (a.rows + kRowsPerWave - 1) / kRowsPerWave;
+    const int64_t blocks = (waves + kWaves - 1) / kWaves;
     if (blocks >= (int64_t(1) << 31) / (64 * kWaves)) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(scan_kernel, dim3((unsigned)blocks), dim3(64 * kWaves), 0, stream, a);
     return hipGetLastError();
