@@ -272,13 +272,16 @@ int givens_emu_batched(int n, int i, int j,
  * Batched inclusive scan through a rule-built matrix (Sec. 4.1, eq.
  * scan-mat): for every row r in [0, rows),
  *   Y[r][j] := sum_{i <= j} X[r][i],   j in [0, len)
- * computed as the product of the row with the upper-triangular all-ones
- * matrix U (u_ij = 1 for i <= j), whose operand fragments are generated from
- * that rule with foreach_ij, in emulated FP32 (Sec. 4.4) on 64-column chunks
- * chained by an FP32 running total.  X: rows x len, row stride ldx >=
- * max(1, len); Y likewise with ldy.  Y may be X itself (ldy == ldx) for an
- * in-place scan; any other overlap is an error.  Rows are independent; a
- * wavefront scans 32 rows, so parallelism comes from the number of rows.
+ computed with the upper-triangular all-ones matrix U (u_ij = 1 for
+ * i <= j), whose operand fragments are generated from that rule with
+ * foreach_ij, in emulated FP32 (Sec. 4.4): each block of 1024 values is
+ * taken as 32 segments of 32, scanned within segments by one product with
+ * U's 32 x 32 block, and the segments and blocks are chained by FP32 running
+ * totals.  X: rows x len, row stride ldx >= max(1, len); Y likewise with
+ * ldy.  Y may be X itself (ldy == ldx) for an in-place scan; any other
+ * overlap is an error.  Rows are independent; a wavefront scans 8 rows, so
+ * parallelism comes from the number of rows.  Rows of a multiple of 1024
+ * values with 16-byte aligned X and Y rows take 16-byte accesses.
  * Supported: rows < 2^30 (else SGEMM_EMU_ERR_UNSUPPORTED).
  * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL, _ALIAS, _UNSUPPORTED, _HIP.
  */

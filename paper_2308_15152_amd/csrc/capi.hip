@@ -404,7 +404,8 @@ int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx, float* Y,
     a.ldx = ldx;
     a.Y = Y;
     a.ldy = ldy;
-    a.vec = ((uintptr_t)X % 16 == 0) && ldx % 4 == 0;
+    // 16-byte loads of X and 16-byte stores of Y
+    a.vec = ((uintptr_t)X % 16 == 0) && ldx % 4 == 0 && ((uintptr_t)Y % 16 == 0) && ldy % 4 == 0;
     hipError_t e = sgemm_emu::launch_scan(a, stream);
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }

@@ -97,7 +97,7 @@ struct ScanArgs {
     int64_t ldx;
     float* Y;
     int64_t ldy;
-    bool vec;  // X 16-byte aligned with ldx a multiple of 4
+    bool vec;  // X and Y 16-byte aligned, ldx and ldy multiples of 4
 };
 
 hipError_t launch_scan(const ScanArgs& a, hipStream_t stream);

@@ -84,6 +84,20 @@ def test_padded_and_unaligned(offset, length, pitch):
     assert np.all(out[:, length:] == 5.0)
 
 
+def test_unaligned_output_only():
+    """X aligned, Y one element off 16-byte alignment: the 16-byte stores of
+    the whole-block path must not be used."""
+    dev = device()
+    X = synth.uniform((9, 2048), synth.rng(7)).to(dev)
+    ybuf = torch.full((9 * 2048 + 1,), 5.0, device=dev)
+    Y = ybuf[1:].view(9, 2048)
+    pkg.sgemm_emu_scan(X, Y)
+    out = to_np(ybuf)
+    assert out[0] == 5.0
+    gate(out[1:].reshape(9, 2048), oracle.scan(to_np(X)), _k_eff(2048), "scan unaligned Y",
+         max_gate=False)
+
+
 def test_workload_scan_sampled():
     w = synth.WORKLOADS["scan_2048"]
     print(f"case workload=scan_2048 rows={w.batch} len={w.n}", flush=True)
