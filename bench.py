@@ -69,10 +69,18 @@ KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are ad
 }
 
 
+def _code_text(text: str) -> str:
+    """Source text with comments removed and whitespace collapsed, so that a
+    change to comments alone does not count as a change of the kernel."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash(kernel: str) -> str:
-    """SHA-256 over the sources a kernel is built from: its translation unit
-    and every header it includes (transitively, quoted includes found in the
-    package's csrc/ or in include/)."""
+    """SHA-256 over the code (comments and layout ignored) a kernel is built
+    from: its translation unit and every header it includes (transitively,
+    quoted includes found in the package's csrc/ or in include/)."""
     csrc = os.path.join(ROOT, "paper_2308_15152_amd", "csrc")
     inc = os.path.join(ROOT, "include")
     seen, todo = set(), [os.path.join(csrc, KERNEL_SOURCES[kernel])]
@@ -91,8 +99,8 @@ def kernel_source_hash(kernel: str) -> str:
     h = hashlib.sha256()
     for f in sorted(seen):
         h.update(os.path.relpath(f, ROOT).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f) as fh:
+            h.update(_code_text(fh.read()).encode())
     return h.hexdigest()
 
 

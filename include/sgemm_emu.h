@@ -189,9 +189,11 @@ int sgemm_emu_resolve_policy(int m, int n, int k,
  * MFMAE_SHAPE_32x32x16), ec the policy: 1 = error correction (3 products),
  * 0 = hi.hi only.  16-byte accesses are used along each operand's contiguous
  * direction when its base is 16-byte aligned and its ld and stride are
- * multiples of 4; any alignment is accepted.
+ * multiples of 4; any alignment is accepted.  Supported: m, n, k < 2^30
+ * (else SGEMM_EMU_ERR_UNSUPPORTED).
  * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL (A or B NULL with k > 0, D NULL),
- * _STRIDE, _ALIAS, _POLICY (op, layout, shape or ec out of range), _HIP.
+ * _STRIDE, _ALIAS, _POLICY (op, layout, shape or ec out of range),
+ * _UNSUPPORTED, _HIP.
  */
 #define SGEMM_EMU_OP_N 0
 #define SGEMM_EMU_OP_T 1

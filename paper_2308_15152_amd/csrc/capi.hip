@@ -267,6 +267,8 @@ int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k
     if (!ld_ok(lda, ac) || !ld_ok(ldb, bc) || !ld_ok(ldd, cc) || (C && !ld_ok(ldc, cc)))
         return SGEMM_EMU_ERR_LD;
     if (m == 0 || n == 0 || batch == 0) return SGEMM_EMU_OK;
+    // tile and k-step indices are formed in 32 bits with room for one tile
+    if (m >= (1 << 30) || n >= (1 << 30) || k >= (1 << 30)) return SGEMM_EMU_ERR_UNSUPPORTED;
     if (D == nullptr || (k > 0 && (A == nullptr || B == nullptr))) return SGEMM_EMU_ERR_NULL;
     if (stride.a < 0 || stride.b < 0 || stride.c < 0 || stride.d < 0) return SGEMM_EMU_ERR_STRIDE;
     if (batch > 1 && stride.d < (int64_t)(cr - 1) * ldd + cc) return SGEMM_EMU_ERR_STRIDE;

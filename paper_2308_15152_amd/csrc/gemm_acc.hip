@@ -39,13 +39,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void gemm_acc_kernel(AccArgs p, int
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t task = task0 + (int64_t)blockIdx.x * kWaves + wave;
     if (task >= task0 + ntasks) return;  // whole wave; no barrier below
-    const int tiles_m = (p.m + 2 * M - 1) / (2 * M);
-    const int tiles_n = (p.n + 2 * N - 1) / (2 * N);
-    const int64_t per_item = (int64_t)tiles_m * tiles_n;
+    const int64_t tiles_m = ((int64_t)p.m + 2 * M - 1) / (2 * M);
+    const int64_t tiles_n = ((int64_t)p.n + 2 * N - 1) / (2 * N);
+    const int64_t per_item = tiles_m * tiles_n;
     const int64_t item = task / per_item;
-    const int t = (int)(task - item * per_item);
-    const int m0 = (t / tiles_n) * 2 * M;
-    const int n0 = (t % tiles_n) * 2 * N;
+    const int64_t t = task - item * per_item;
+    const int m0 = (int)(t / tiles_n) * 2 * M;
+    const int n0 = (int)(t % tiles_n) * 2 * N;
 
     const float* Ai = p.A + item * p.sa;
     const float* Bi = p.B + item * p.sb;
@@ -116,7 +116,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void gemm_acc_kernel(AccArgs p, int
 
 template <int M, int N, int K, bool EC, class LA, class LB>
 hipError_t launch_acc_cfg(const AccArgs& a, hipStream_t stream) {
-    const int64_t tiles = (int64_t)((a.m + 2 * M - 1) / (2 * M)) * ((a.n + 2 * N - 1) / (2 * N));
+    const int64_t tiles =
+        (((int64_t)a.m + 2 * M - 1) / (2 * M)) * (((int64_t)a.n + 2 * N - 1) / (2 * N));
     const int64_t total = tiles * a.batch;
     // one launch stays below 2^31 work-items
     const int64_t max_tasks = ((int64_t(1) << 31) / (64 * kWaves) - 1) * kWaves;

@@ -290,6 +290,8 @@ def test_batched_acc_validation():
     assert acc(lay=1, ldc=64, ldd=64) == -4
     assert acc(m=0) == 0
     assert acc(batch=0) == 0
+    assert acc(m=1 << 30, lda=1 << 30) == -6
+    assert acc(k=1 << 30, lda=1 << 30) == -6
     assert acc(D=0) == -3
     assert acc(A=0) == -3
     assert acc(B=0) == -3

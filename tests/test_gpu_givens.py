@@ -124,3 +124,24 @@ def test_workload_givens_sampled(mode):
     ref = oracle.givens(i, j, c.numpy(), s.numpy(), B.numpy(), items=items)
     e = gate(C[items], ref, K_EFF, f"givens_64 {mode}", max_gate=False)
     print(f"givens_64 {mode}: err {e[0]:.3e} fp32 {e[1]:.3e}")
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_broadcast_angle_single_item_and_column_groups(mode):
+    """One (c, s) for every item (stride 0), a single item, and 200 columns
+    (four column groups, the last partial, odd pairing off)."""
+    dev = device()
+    i, j = (62, 63) if mode == "embedded" else (9, 50)
+    c, s, B = synth.givens_inputs(4, 64, 200, seed=91)
+    cb = c[:1].to(dev).expand(4)
+    sb = s[:1].to(dev).expand(4)
+    C = to_np(pkg.givens_emu_batched(i, j, cb, sb, B.to(dev), mode=MODES[mode]))
+    c4 = np.full(4, c[0].item(), np.float32)
+    s4 = np.full(4, s[0].item(), np.float32)
+    gate(C, oracle.givens(i, j, c4, s4, B.numpy()), K_EFF, f"givens broadcast {mode}",
+         max_gate=False)
+    one = to_np(pkg.givens_emu_batched(i, j, c[:1].to(dev), s[:1].to(dev), B[:1, :, :199]
+                                       .contiguous().to(dev), mode=MODES[mode]))
+    gate(one, oracle.givens(i, j, c[:1].numpy(), s[:1].numpy(),
+                            np.ascontiguousarray(B[:1, :, :199].numpy())), K_EFF,
+         f"givens single {mode}", max_gate=False)
