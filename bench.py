@@ -62,6 +62,7 @@ KERNEL_SOURCES = {  # the translation unit of each kernel; shared headers are ad
     "bgemm_big_stream_kernel": "bgemm_big.hip",
     "bgemm_emu_kernel": "bgemm.hip",
     "householder64_kernel": "rulebuilt.hip",
+    "householder64_lds_kernel": "rulebuilt.hip",
     "givens64_kernel": "rulebuilt.hip",
     "givens64_lds_kernel": "rulebuilt.hip",
     "gemm_acc_kernel": "gemm_acc.hip",
@@ -138,6 +139,9 @@ def parse():
                     help="how a Givens workload builds G: map with (i, j) as kernel "
                          "arguments, map with (i, j) compiled in, G stored in LDS, or the "
                          "library's choice")
+    ap.add_argument("--householder-mode", default="rule", choices=["rule", "lds"],
+                    help="Householder workload: reflector built in registers (rule) or the "
+                         "baseline through LDS")
     ap.add_argument("--batch", type=int, default=None,
                     help="override the workload's batch size (a measurement variant, "
                          "recorded in config; the default line uses the workload's own)")
@@ -168,7 +172,7 @@ def copy_calibration(steps: int):
                       "ms_per_copy": dt * 1e3, "GBps": 8 * n / dt / 1e9}), flush=True)
 
 
-def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO):
+def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO, hh_mode=pkg.HOUSEHOLDER_RULE):
     if w.kind == "givens":
         c, s, B = inputs
         C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
@@ -196,7 +200,7 @@ def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO):
         C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
 
         def call():
-            pkg.householder_emu_batched(u, B, C)
+            pkg.householder_emu_batched(u, B, C, mode=hh_mode)
         return call, C
     A, B = inputs
     C = torch.empty((w.batch, w.m, w.n), dtype=torch.float32, device="cuda")
@@ -358,7 +362,8 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     if (args.flow, args.ec, args.tile) != (pkg.FLOW_AUTO, 1, pkg.TILE_AUTO):
         policy = pkg.Policy(args.flow, args.ec, args.tile)
     givens_mode = GIVENS_MODES[args.givens_mode]
-    call, C = make_call(w, dev_inputs, policy, givens_mode)
+    hh_mode = pkg.HOUSEHOLDER_LDS if args.householder_mode == "lds" else pkg.HOUSEHOLDER_RULE
+    call, C = make_call(w, dev_inputs, policy, givens_mode, hh_mode)
 
     for _ in range(args.warmup):
         call()
@@ -397,7 +402,8 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         roof = {"bound": "hbm", "achieved": bytes_alg / (ms_step * 1e-3) / 1e9,
                 "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    resolved, kernel = None, "householder64_kernel"
+    resolved, kernel = None, ("householder64_lds_kernel" if hh_mode == pkg.HOUSEHOLDER_LDS
+                              else "householder64_kernel")
     if w.kind == "givens":
         kernel = "givens64_lds_kernel" if givens_mode == pkg.GIVENS_LDS else "givens64_kernel"
     elif w.kind == "gemm_acc":
@@ -411,6 +417,8 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     tkey = w.name
     if w.kind == "givens" and args.givens_mode != "auto":
         tkey += ":" + args.givens_mode
+    if w.kind == "householder" and args.householder_mode != "rule":
+        tkey += ":" + args.householder_mode
     if w.batch != synth.WORKLOADS[name].batch:
         tkey += f":batch{w.batch}"
     roof["traffic"] = measured_traffic(tkey, roof["kernel"])
@@ -434,7 +442,9 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
                    {"flow": resolved.flow, "ec": resolved.ec, "tile": resolved.tile,
                     "requested": "auto" if policy is None else "explicit"},
                    **({"givens": {"plane": list(w.plane), "mode": args.givens_mode}}
-                      if w.kind == "givens" else {})},
+                      if w.kind == "givens" else {}),
+                   **({"householder_mode": args.householder_mode}
+                      if w.kind == "householder" else {})},
         "frac_fp32_vector_peak": tflops / PEAK_FP32_VECTOR_TFLOPS,
         "frac_fp16_mfma_over_3": tflops / (PEAK_FP16_MFMA_TFLOPS / 3),
         "hbm_GBps_algorithmic": bytes_alg / (ms_step * 1e-3) / 1e9,

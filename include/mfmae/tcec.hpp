@@ -33,13 +33,34 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 // is rounded once, to binary16 -- the same two roundings as the definition.
 // (gfx950 evaluates the fma with hi read straight from its binary16 register,
 // v_fma_mix, so the residual costs two instructions.)
+//
+// x must be an FP32 value the compiler cannot re-derive from a wider
+// intermediate: a value loaded from memory, say.  For the result of FP32
+// arithmetic just before the split use split_rounded.
 __device__ inline void split(float x, _Float16& hi, _Float16& lo) {
     hi = static_cast<_Float16>(x);
     lo = static_cast<_Float16>(__builtin_fmaf(static_cast<float>(hi), -kLoScale, x * kLoScale));
 }
 
+// The split is defined on the FP32 value.  The empty asm keeps x in a VGPR
+// as that value, so the compiler cannot fold the rounding that produced x
+// into the conversion: fptrunc(fma(a, b, c)) is otherwise selected as one
+// v_fma_mix with a single rounding of the exact a b + c, which differs from
+// toFP16(fl32(a b + c)) when fl32(a b + c) is a binary16 tie (the fold is
+// made whatever the contraction setting).
+__device__ inline float as_fp32(float x) {
+    __asm__("" : "+v"(x));
+    return x;
+}
+
+// split of a value computed by FP32 arithmetic (a rule-built entry).
+__device__ inline void split_rounded(float x, _Float16& hi, _Float16& lo) {
+    split(as_fp32(x), hi, lo);
+}
+
 // Split two values: hi is converted as a pair (one v_cvt_pk_f16_f32) and the
-// two residuals read their hi halves from that packed register.
+// two residuals read their hi halves from that packed register.  Same
+// condition on x0, x1 as for split.
 __device__ inline void split_pair(float x0, float x1, half2_t& hi, half2_t& lo) {
     hi = __builtin_convertvector(f32x2_t{x0, x1}, half2_t);
     lo[0] = static_cast<_Float16>(
@@ -117,7 +138,7 @@ __device__ inline void build(frag_emu<S, U>& f, Fn&& value) {
 #pragma unroll
     for (int e = 0; e < L::num_elements; ++e) {
         _Float16 h, lo;
-        split(value(L::row(l, e), L::col(l, e)), h, lo);
+        split_rounded(value(L::row(l, e), L::col(l, e)), h, lo);
         f.hi[e] = h;
         f.lo[e] = lo;
     }

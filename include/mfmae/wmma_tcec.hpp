@@ -118,11 +118,12 @@ struct fragment<accumulator, M, N, K, float, void, Policy> {
 
 // ---- element access -------------------------------------------------------
 
-// Operand element e of this lane := x (split into hi and lo).
+// Operand element e of this lane := x (split into hi and lo; x may be the
+// result of FP32 arithmetic, e.g. an entry built from a rule).
 template <class F>
 __device__ inline void set_element(F& f, int e, float x) {
     _Float16 h, l;
-    mfmae::tcec::split(x, h, l);
+    mfmae::tcec::split_rounded(x, h, l);
     f.hi[e] = h;
     f.lo[e] = l;
 }
@@ -165,7 +166,7 @@ __host__ __device__ constexpr void map(int& lane, int& elem, int i, int j) {
 template <class UseT, int M, int N, int K, class L, class P>
 __device__ inline void fill_fragment(fragment<UseT, M, N, K, float, L, P>& f, float v) {
     _Float16 h, l;
-    mfmae::tcec::split(v, h, l);
+    mfmae::tcec::split_rounded(v, h, l);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         f.hi[e] = h;

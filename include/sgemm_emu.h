@@ -230,6 +230,22 @@ int householder_emu_batched(int n, const float* u, int64_t stride_u,
                             float* C, int ldc, int64_t stride_c,
                             int batch, hipStream_t stream);
 
+/* householder_emu_batched with a choice of how the reflector's fragments are
+ * built (the comparison of Sec. 4.2.1):
+ *   SGEMM_EMU_HOUSEHOLDER_RULE  in registers by foreach_ij (as above);
+ *   SGEMM_EMU_HOUSEHOLDER_LDS   baseline: every entry of H is formed once,
+ *                               split and written to LDS (16 KiB per wave),
+ *                               and the fragments are loaded from there.
+ * Both form the same entries and give bit-identical results.  Extra error:
+ * SGEMM_EMU_ERR_POLICY for an unknown mode. */
+#define SGEMM_EMU_HOUSEHOLDER_RULE 0
+#define SGEMM_EMU_HOUSEHOLDER_LDS 1
+
+int householder_emu_batched_ex(int n, const float* u, int64_t stride_u,
+                               const float* B, int ldb, int64_t stride_b, int ncols,
+                               float* C, int ldc, int64_t stride_c,
+                               int batch, int mode, hipStream_t stream);
+
 /*
  * Batched Givens rotation with the rotation matrix built in registers
  * (Sec. 4.3.1):

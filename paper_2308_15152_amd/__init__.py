@@ -20,9 +20,10 @@ __all__ = [
     "SgemmEmuError", "lib_path", "load",
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
     "sgemm_emu_batched_acc", "sgemm_emu_scan",
-    "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
-    "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
-    "sgemm_emu_last_hip_error",
+    "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
+    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
+    "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+    "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS",
     "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
@@ -40,15 +41,16 @@ SHAPE_16x16x32, SHAPE_32x32x16 = 0, 1
 USE_A, USE_B, USE_ACC = 0, 1, 2
 GIVENS_AUTO, GIVENS_MAP, GIVENS_EMBEDDED, GIVENS_LDS = 0, 1, 2, 3
 OP_N, OP_T = 0, 1
+HOUSEHOLDER_RULE, HOUSEHOLDER_LDS = 0, 1
 ROW_MAJOR, COL_MAJOR = 0, 1
 
 # Every symbol declared in include/sgemm_emu.h.
 EXPORTED_SYMBOLS = (
     "sgemm_emu_batched", "sgemm_emu_batched_ex", "sgemm_emu_resolve_policy",
     "sgemm_emu_batched_acc", "sgemm_emu_scan",
-    "householder_emu_batched", "givens_emu_batched", "sgemm_emu_split", "mfmae_num_elements",
-    "mfmae_map", "mfmae_foreach", "mfmae_mma_probe", "sgemm_emu_strerror",
-    "sgemm_emu_last_hip_error",
+    "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
+    "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
+    "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
 )
 
 
@@ -109,6 +111,8 @@ def load():
                                    i32, Stride4, i32, i32, P], i32),
         "sgemm_emu_scan": ([i64, i32, P, i64, P, i64, P], i32),
         "householder_emu_batched": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, P], i32),
+        "householder_emu_batched_ex": ([i32, P, i64, P, i32, i64, i32, P, i32, i64, i32, i32, P],
+                                       i32),
         "givens_emu_batched": ([i32, i32, i32, P, P, i64, P, i32, i64, i32, P, i32, i64, i32,
                                 i32, P], i32),
         "sgemm_emu_split": ([i64, P, P, P, P], i32),
@@ -322,8 +326,10 @@ def sgemm_emu_scan(X, Y=None, *, stream=None):
     return Y
 
 
-def householder_emu_batched(u, B, C=None, *, stream=None):
-    """C[t] := (I - 2 u[t] u[t]^T) @ B[t]; u: [batch, 64], B: [batch, 64, ncols]."""
+def householder_emu_batched(u, B, C=None, *, mode: int = HOUSEHOLDER_RULE, stream=None):
+    """C[t] := (I - 2 u[t] u[t]^T) @ B[t]; u: [batch, 64], B: [batch, 64, ncols].
+    mode: HOUSEHOLDER_RULE (reflector built in registers) or HOUSEHOLDER_LDS
+    (baseline through LDS)."""
     import torch
 
     if u.dtype != torch.float32 or not u.is_cuda or u.dim() != 2:
@@ -338,10 +344,14 @@ def householder_emu_batched(u, B, C=None, *, stream=None):
         C = torch.empty((batch, n, ncols), dtype=torch.float32, device=u.device)
     _, _, _, ldc, sc = _matrix_view(C, "C")
     su = u.stride(0) if batch > 1 else 0
-    rc = load().householder_emu_batched(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C), ldc,
-                                        sc, batch, _stream(stream))
-    _check(rc, "householder_emu_batched")
+    rc = load().householder_emu_batched_ex(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C),
+                                           ldc, sc, batch, int(mode), _stream(stream))
+    _check(rc, "householder_emu_batched_ex")
     return C
+
+
+def householder_emu_batched_ex(u, B, C=None, *, mode: int, stream=None):
+    return householder_emu_batched(u, B, C, mode=mode, stream=stream)
 
 
 def givens_emu_batched(i, j, c, s, B, C=None, *, mode: int = GIVENS_AUTO, stream=None):

@@ -317,6 +317,15 @@ int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k
 int householder_emu_batched(int n, const float* u, int64_t stride_u, const float* B, int ldb,
                             int64_t stride_b, int ncols, float* C, int ldc, int64_t stride_c,
                             int batch, hipStream_t stream) {
+    return householder_emu_batched_ex(n, u, stride_u, B, ldb, stride_b, ncols, C, ldc, stride_c,
+                                      batch, SGEMM_EMU_HOUSEHOLDER_RULE, stream);
+}
+
+int householder_emu_batched_ex(int n, const float* u, int64_t stride_u, const float* B, int ldb,
+                               int64_t stride_b, int ncols, float* C, int ldc, int64_t stride_c,
+                               int batch, int mode, hipStream_t stream) {
+    if (mode != SGEMM_EMU_HOUSEHOLDER_RULE && mode != SGEMM_EMU_HOUSEHOLDER_LDS)
+        return SGEMM_EMU_ERR_POLICY;
     if (n < 0 || ncols < 0 || batch < 0) return SGEMM_EMU_ERR_DIM;
     if (ldb < (ncols > 1 ? ncols : 1) || ldc < (ncols > 1 ? ncols : 1)) return SGEMM_EMU_ERR_LD;
     if (n == 0 || ncols == 0 || batch == 0) return SGEMM_EMU_OK;
@@ -331,6 +340,7 @@ int householder_emu_batched(int n, const float* u, int64_t stride_u, const float
     const Extent eb = extent(B, stride_b == 0 ? 1 : batch, n, ncols, ldb, stride_b);
     if (overlap(ec, eu) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
     sgemm_emu::HouseholderArgs a;
+    a.mode = mode;
     a.ncols = ncols;
     a.u = u;
     a.su = stride_u;

@@ -40,6 +40,7 @@ hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t st
 bool big_streams(const GemmArgs& a, int tile, int flow);
 
 struct HouseholderArgs {
+    int mode;  // SGEMM_EMU_HOUSEHOLDER_RULE or _LDS
     int ncols;
     const float* u;
     int64_t su;

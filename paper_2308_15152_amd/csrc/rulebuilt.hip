@@ -8,7 +8,8 @@
 //     Per 16-wide k step one foreach_ij over the A-operand map fills both
 //     32-row blocks (the index computation is shared by the two fragments,
 //     and -2 u_i of the lane's rows is computed once), which is what keeps
-//     rule-built fragments cheaper than a trip through memory.
+//     rule-built fragments cheaper than a trip through memory.  The baseline
+//     forms every entry once into LDS and loads the fragments from there.
 //   Givens (Sec. 4.3.1; map of Sec. 4.3):
 //     C = G(i, j, theta) B with G the identity except G_ii = G_jj = c,
 //     G_ij = -s, G_ji = s.  The fragments are filled with zeros and the
@@ -92,7 +93,7 @@ struct HouseholderRule {
             for (int tm = 0; tm < 2; ++tm) {
                 const float h = __builtin_fmaf(urow[tm], uj, (32 * tm + i) == gj ? 1.0f : 0.0f);
                 _Float16 vh, vl;
-                mfmae::tcec::split(h, vh, vl);
+                mfmae::tcec::split_rounded(h, vh, vl);
                 hh[tm][e] = vh;
                 hl[tm][e] = vl;
             }
@@ -161,21 +162,41 @@ struct GivensMapRule {
     }
 };
 
-// Givens rotation, baseline: the wave writes G (hi and lo planes) to its
-// own 16 KiB of LDS and loads the fragments from there.  Rows of 64 halves
-// (128 bytes, 8 pieces of 8 halves); piece p of row r is stored at
-// position p ^ ((r ^ (r >> 3)) & 7), so that the 32 rows a fragment load
-// touches spread over all banks.
-struct GivensLdsRule {
+// Baselines: the left matrix is written to the wave's own 16 KiB of LDS
+// (hi and lo planes) and the fragments are loaded from there, as a fragment
+// API without rule-built fragments requires.  Rows of 64 halves (128 bytes,
+// 8 pieces of 8 halves); piece p of row r is stored at position
+// p ^ ((r ^ (r >> 3)) & 7), so that the 32 rows a fragment load touches
+// spread over all banks.
+struct LdsOperand {
     unsigned char* hi;  // [64 rows][128 bytes]
     unsigned char* lo;
 
     __device__ static int off(int r, int p) { return r * 128 + 16 * (p ^ ((r ^ (r >> 3)) & 7)); }
 
-    __device__ void init(const RuleParams& p, int64_t item, unsigned char* lds) {
-        const int l = threadIdx.x & 63;
+    __device__ void bind(unsigned char* lds) {
         hi = lds;
         lo = lds + 64 * 128;
+    }
+
+    __device__ void build(int s, half8_t (&hh)[2], half8_t (&hl)[2]) const {
+        const int l = threadIdx.x & 63;
+        const int p = 2 * s + (l >> 5);  // k = 16 s + 8 (l / 32) + e
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+            const int o = off(32 * tm + (l & 31), p);
+            hh[tm] = *reinterpret_cast<const half8_t*>(hi + o);
+            hl[tm] = *reinterpret_cast<const half8_t*>(lo + o);
+        }
+    }
+};
+
+// Givens baseline: zero both planes, then lane r writes G_rr (c at i and j,
+// else 1) and lanes 0 and 1 the two off-diagonal entries.
+struct GivensLdsRule : LdsOperand {
+    __device__ void init(const RuleParams& p, int64_t item, unsigned char* lds) {
+        const int l = threadIdx.x & 63;
+        bind(lds);
         const float c = p.c[item * p.scs];
         const float s = p.s[item * p.scs];
         // zero both planes: 64 rows x 8 pieces, 8 pieces per lane
@@ -186,10 +207,9 @@ struct GivensLdsRule {
             *reinterpret_cast<half8_t*>(hi + off(piece >> 3, piece & 7)) = z;
             *reinterpret_cast<half8_t*>(lo + off(piece >> 3, piece & 7)) = z;
         }
-        // lane r writes G_rr (c at i and j, else 1); lanes 0 and 1 the two
-        // off-diagonal entries.  A wave's LDS accesses complete in the order
-        // they are issued; the fences keep the compiler from reordering the
-        // zeros, these entries and the loads in build().
+        // A wave's LDS accesses complete in the order they are issued; the
+        // fences keep the compiler from reordering the zeros, these entries
+        // and the loads in build().
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
         auto put = [&](int r, int q, float v) {
             _Float16 vh, vl;
@@ -203,16 +223,33 @@ struct GivensLdsRule {
         if (l == 1) put(p.gj, p.gi, s);
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
+};
 
-    __device__ void build(int s, half8_t (&hh)[2], half8_t (&hl)[2]) const {
+// Householder baseline: every entry h_ij = fmaf(-2 u_i, u_j, delta_ij) is
+// formed once, split, and written to LDS; lane l forms 8 pieces of 8
+// entries (rows (64 t + l) / 8, t = 0..7).
+struct HouseholderLdsRule : LdsOperand {
+    __device__ void init(const RuleParams& p, int64_t item, unsigned char* lds) {
         const int l = threadIdx.x & 63;
-        const int p = 2 * s + (l >> 5);  // k = 16 s + 8 (l / 32) + e
+        bind(lds);
+        const float* u = p.u + item * p.su;
 #pragma unroll
-        for (int tm = 0; tm < 2; ++tm) {
-            const int o = off(32 * tm + (l & 31), p);
-            hh[tm] = *reinterpret_cast<const half8_t*>(hi + o);
-            hl[tm] = *reinterpret_cast<const half8_t*>(lo + o);
+        for (int t = 0; t < 8; ++t) {
+            const int piece = 64 * t + l;
+            const int r = piece >> 3, q0 = 8 * (piece & 7);
+            const float ur = -2.0f * u[r];
+            float h[8];
+#pragma unroll
+            for (int v = 0; v < 8; ++v)
+                h[v] = mfmae::tcec::as_fp32(
+                    __builtin_fmaf(ur, u[q0 + v], (r == q0 + v) ? 1.0f : 0.0f));
+            half8_t vh, vl;
+            mfmae::tcec::split8(h, vh, vl);
+            *reinterpret_cast<half8_t*>(hi + off(r, piece & 7)) = vh;
+            *reinterpret_cast<half8_t*>(lo + off(r, piece & 7)) = vl;
         }
+        // the fragment loads in build() read what other lanes wrote
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
 };
 
@@ -329,6 +366,12 @@ __global__ __launch_bounds__(64 * kWaves, 2) void householder64_kernel(RuleParam
     rule64_body<HouseholderRule, PAIR>(p, nullptr);
 }
 
+template <bool PAIR>
+__global__ __launch_bounds__(64 * kWaves, 2) void householder64_lds_kernel(RuleParams p) {
+    __shared__ __attribute__((aligned(16))) unsigned char lds[kWaves][2 * 64 * 128];
+    rule64_body<HouseholderLdsRule, PAIR>(p, lds[threadIdx.x >> 6]);
+}
+
 template <bool EMBED, int I, int J, bool PAIR>
 __global__ __launch_bounds__(64 * kWaves, 2) void givens64_kernel(RuleParams p) {
     rule64_body<GivensMapRule<EMBED, I, J>, PAIR>(p, nullptr);
@@ -400,9 +443,12 @@ hipError_t launch_householder64(const HouseholderArgs& a, hipStream_t stream) {
     p.C = a.C;
     p.ldc = a.ldc;
     p.sc = a.sc;
-    if (pairs_ok(a.B, a.ldb, a.sb, a.C, a.ldc, a.sc, a.ncols))
-        return launch_rule(householder64_kernel<true>, p, a.batch, stream);
-    return launch_rule(householder64_kernel<false>, p, a.batch, stream);
+    const bool pair = pairs_ok(a.B, a.ldb, a.sb, a.C, a.ldc, a.sc, a.ncols);
+    if (a.mode == SGEMM_EMU_HOUSEHOLDER_LDS)
+        return pair ? launch_rule(householder64_lds_kernel<true>, p, a.batch, stream)
+                    : launch_rule(householder64_lds_kernel<false>, p, a.batch, stream);
+    return pair ? launch_rule(householder64_kernel<true>, p, a.batch, stream)
+                : launch_rule(householder64_kernel<false>, p, a.batch, stream);
 }
 
 hipError_t launch_givens64(const GivensArgs& a, hipStream_t stream) {

@@ -30,6 +30,13 @@ def test_header_declarations_match_binding():
     assert _declared_functions() == sorted(pkg.EXPORTED_SYMBOLS)
 
 
+def test_binding_defines_every_public_name():
+    for name in pkg.__all__:
+        assert hasattr(pkg, name), name
+    for name in pkg.EXPORTED_SYMBOLS:
+        assert callable(getattr(pkg, name, None)), name
+
+
 def test_library_exports_every_declared_symbol():
     lib = pkg.load()
     for name in _declared_functions():
@@ -212,6 +219,11 @@ def test_householder_validation():
     assert hh(C=PA + 4) == -5
     assert hh(batch=0) == 0
     assert hh(ncols=0) == 0
+    for mode in (-1, 2):
+        assert lib.householder_emu_batched_ex(64, P(PA), 64, P(PB), 64, 4096, 64, P(PC), 64,
+                                              4096, 2, mode, P(0)) == -8
+    assert lib.householder_emu_batched_ex(64, P(0), 64, P(PB), 64, 4096, 64, P(PC), 64, 4096,
+                                          2, 1, P(0)) == -3
 
 
 def test_givens_validation():

@@ -1,13 +1,17 @@
 """Parity of the batched Householder application C = (I - 2 u u^T) B with the
 reflector built in registers (Sec. 4.2.1) in emulated FP32 (Sec. 4.4).
 
-* the reflector entries the kernel forms are fmaf(-2 u_i, u_j, delta_ij),
-  bit for bit: with B = I every output is hi(h) + lo(h) 2^-11 rounded once,
-  which the oracle computes from its own split of H32;
+* the reflector entries the kernel forms are fmaf(-2 u_i, u_j, delta_ij):
+  with B = I every output is hi(h) + lo(h) 2^-11 rounded once, which the
+  oracle computes from its own split of H32 (this pins h and the split up
+  to pairs (hi, lo) that reconstruct the same value); a constructed binary16
+  tie pins the split of the FP32 entry itself;
 * the accuracy gate against the FP64 product and the plain FP32 product;
 * u = +-e_i flips one row of B exactly up to the split of B;
 * ragged column counts and padded leading dimensions;
-* the full-size workload on sampled items.
+* the full-size workload on sampled items;
+* the baseline that forms H in LDS (the comparison of Sec. 4.2.1) places
+  the same entries: bit-identical to the register-built reflector.
 """
 import numpy as np
 import pytest
@@ -21,9 +25,9 @@ from gpu_util import device, gate, to_np
 pytestmark = pytest.mark.gpu
 
 
-def _run(u, B, C=None):
+def _run(u, B, C=None, mode=pkg.HOUSEHOLDER_RULE):
     dev = device()
-    return to_np(pkg.householder_emu_batched(u.to(dev), B.to(dev), C))
+    return to_np(pkg.householder_emu_batched(u.to(dev), B.to(dev), C, mode=mode))
 
 
 def test_reflector_entries_bit_exact():
@@ -83,3 +87,47 @@ def test_workload_householder_sampled():
     ref = oracle.householder(u.numpy(), B.numpy(), items=items)
     e = gate(C[items], ref, 64, "householder_64")
     print(f"householder_64: err {e[0]:.3e} fp32 {e[1]:.3e}")
+
+
+@pytest.mark.parametrize("ncols", [64, 33, 130])
+def test_lds_baseline_bit_identical(ncols):
+    u, B = synth.householder_inputs(7, 64, ncols, seed=51 + ncols)
+    reg = _run(u, B)
+    lds = _run(u, B, mode=pkg.HOUSEHOLDER_LDS)
+    assert np.array_equal(reg.view(np.uint32), lds.view(np.uint32))
+    gate(lds, oracle.householder(u.numpy(), B.numpy()), 64, f"householder lds ncols={ncols}")
+
+
+def test_lds_baseline_reflector_entries():
+    u, _ = synth.householder_inputs(4, 64, 64, seed=52)
+    eye = torch.eye(64).expand(4, 64, 64).contiguous()
+    C = _run(u, eye, mode=pkg.HOUSEHOLDER_LDS)
+    for b in range(4):
+        hi, lo = oracle.split(oracle.householder_h32(u[b].numpy()))
+        rec = (hi.view(np.float16).astype(np.float32) +
+               lo.view(np.float16).astype(np.float32) * np.float32(2.0 ** -11))
+        assert np.array_equal(C[b].view(np.uint32), rec.astype(np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("mode", [pkg.HOUSEHOLDER_RULE, pkg.HOUSEHOLDER_LDS])
+def test_reflector_split_of_a_binary16_tie(mode):
+    """h_01 = fl32(-2 u_0 u_1) = 1 + 2^-11 is a binary16 tie while the exact
+    product lies just above it: the split of the FP32 entry takes hi = 1
+    (ties to even), lo = 1; rounding the exact product to binary16 in one
+    step (a fused multiply-add with a binary16 result) would give hi = 1 +
+    2^-10, lo = -1, which reconstructs the same value.  With B rows
+    (2^-22, 2 - 2^-10) the two splits give different sums: row 0 of C must
+    equal the method model rounded to FP32."""
+    u = torch.zeros((1, 64))
+    u[0, 0] = -0.5 * (1 + 2.0 ** -23)
+    u[0, 1] = 1 + 4095 * 2.0 ** -23
+    B = torch.zeros((1, 64, 64))
+    B[0, 0, :] = 2.0 ** -22
+    B[0, 1, :] = 2 - 2.0 ** -10
+    h01 = oracle.householder_h32(u[0].numpy())[0, 1]
+    hi, lo = oracle.split(np.array([h01], np.float32))
+    assert h01 == np.float32(1 + 2.0 ** -11)
+    assert hi.view(np.float16)[0] == 1.0 and lo.view(np.float16)[0] == 1.0
+    C = _run(u, B, mode=mode)
+    cm = oracle.householder(u.numpy(), B.numpy(), want=("cm",))["cm"]
+    assert np.array_equal(C[0, 0].view(np.uint32), cm[0, 0].astype(np.float32).view(np.uint32))
