@@ -86,7 +86,17 @@ int sgemm_emu_batched(int m, int n, int k,
  *                         and batch * m * n >= 2048 * 2048, else 256x128,
  *                         else 128x128; otherwise REG for products up to
  *                         1024 x 1024 whose operands allow its vector loads;
- *                         otherwise SPLIT.
+ *                         otherwise, for m and n above 1024 with 16-byte
+ *                         aligned A and B rows, k >= 32 and at least 2^32
+ *                         multiply-adds (batch m n k), the largest of
+ *                         those tiles whose whole tiles cover at least 90%
+ *                         of C: that interior (and k rounded down to a
+ *                         multiple of 32) runs on the full-tile kernel, the
+ *                         remaining k is added to it in place, and the edge
+ *                         strips run on the REG flow with 64 x 64 tiles
+ *                         (when A and the leading dimensions allow it), one
+ *                         launch after another on the stream; otherwise
+ *                         SPLIT.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
  *                         global load and the LDS store; LDS holds hi and lo
  *                         (the same 4 bytes per element as FP32) and the

@@ -67,15 +67,32 @@ int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int
 // Validate, then resolve the policy (flow and tile, AUTO replaced by the
 // library's choice) and fill the kernel arguments.  `launch` is false for an
 // empty problem (nothing to run).
-enum Kernel { K_NONE, K_REG, K_BIG, K_LDS };
+// K_TILED: a large product whose shape does not fill whole tiles, run as
+// its interior of whole tiles on the full-tile kernel, a k tail (k mod 32
+// values) added in place by the accumulate kernel, and the edge strips on
+// the register-flow kernel.
+enum Kernel { K_NONE, K_REG, K_BIG, K_LDS, K_TILED };
 
 const char* kernel_name(Kernel k) {
     switch (k) {
         case K_REG: return "bgemm_reg_kernel";
         case K_BIG: return "bgemm_big_kernel";
         case K_LDS: return "bgemm_emu_kernel";
+        case K_TILED: return "bgemm_big_kernel+bgemm_reg_kernel";
         default: return "";
     }
+}
+
+int tile_rows(int tile) { return tile == SGEMM_EMU_TILE_256x128 ? 256 : 128; }
+int tile_cols(int tile) { return tile == SGEMM_EMU_TILE_128x256 ? 256 : 128; }
+
+// Interior of whole tiles and whole 32-deep k chunks.
+struct Interior {
+    int m, n, k;
+};
+
+Interior interior(const sgemm_emu::GemmArgs& a, int tile) {
+    return {a.m - a.m % tile_rows(tile), a.n - a.n % tile_cols(tile), a.k - a.k % 32};
 }
 
 int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
@@ -131,6 +148,27 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
             tile = reg_tile;
         } else {
             flow = SGEMM_EMU_FLOW_SPLIT;
+            // Large ragged products: whole tiles covering at least 90% of C
+            // run on the full-tile kernel, the k tail on the accumulate
+            // kernel and the edge strips on the register-flow kernel (1.9x
+            // the general kernel's rate on 8000^3 and 6000^3, 1.6x on 2100 x
+            // 2300 x 1000).  Below 2^32 multiply-adds the extra launches
+            // cost more than they gain (measured on 2 x 1500 x 1800 x 544).
+            if (ec == 1 && tile == SGEMM_EMU_TILE_AUTO && a.vec_a && a.vec_b && m > 1024 &&
+                n > 1024 && k >= 32 && (int64_t)batch * m * n * k >= ((int64_t)1 << 32) &&
+                sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_64x64)) {
+                const bool wide = k >= 1024 && (int64_t)m * n * batch >= (int64_t)2048 * 2048;
+                const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
+                                      SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
+                for (int t : order) {
+                    const Interior in = interior(a, t);
+                    if ((int64_t)in.m * in.n * 10 >= (int64_t)m * n * 9) {
+                        tile = t;
+                        kern = K_TILED;
+                        return SGEMM_EMU_OK;
+                    }
+                }
+            }
         }
     }
     if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
@@ -147,6 +185,75 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     return SGEMM_EMU_OK;
 }
 
+// K_TILED, in stream order: the interior C[0:mi, 0:ni] = A[0:mi, 0:ki]
+// B[0:ki, 0:ni] on the full-tile kernel; the k tail C[0:mi, 0:ni] +=
+// A[0:mi, ki:k] B[ki:k, 0:ni] in place; the right strip C[0:mi, ni:n] and
+// the bottom strip C[mi:m, 0:n] over the whole k on the register-flow
+// kernel (64 x 64 tiles).
+// Every piece is a view of the same operands (same ld and item strides).
+// An edge strip (at most one tile deep, long k): the barrier-free register
+// flow on 64 x 64 tiles runs 4-6x faster than the LDS-tiled general kernel
+// there (measured on 7936 x 64 x 8000 and 64 x 8000 x 8000), since the
+// strip has too few tiles to hide the general kernel's per-step barriers.
+// The strips share A's row alignment and both leading dimensions with the
+// whole product, which was checked for this flow before K_TILED was chosen.
+hipError_t run_strip(const sgemm_emu::GemmArgs& s, hipStream_t stream) {
+    return sgemm_emu::launch_gemm_reg(s, SGEMM_EMU_TILE_64x64, true, stream);
+}
+
+hipError_t run_tiled(const sgemm_emu::GemmArgs& a, int tile, hipStream_t stream) {
+    const Interior in = interior(a, tile);
+    sgemm_emu::GemmArgs g = a;
+    g.m = in.m;
+    g.n = in.n;
+    g.k = in.k;
+    hipError_t e = sgemm_emu::launch_gemm_big(g, tile, SGEMM_EMU_FLOW_SPLIT, stream);
+    if (e != hipSuccess) return e;
+    if (in.k < a.k) {
+        sgemm_emu::AccArgs t{};
+        t.m = in.m;
+        t.n = in.n;
+        t.k = a.k - in.k;
+        t.A = a.A + in.k;
+        t.lda = a.lda;
+        t.sa = a.sa;
+        t.B = a.B + (int64_t)in.k * a.ldb;
+        t.ldb = a.ldb;
+        t.sb = a.sb;
+        t.C = a.C;
+        t.ldc = a.ldc;
+        t.sc = a.sc;
+        t.D = a.C;
+        t.ldd = a.ldc;
+        t.sd = a.sc;
+        t.batch = a.batch;
+        t.a_trans = t.b_trans = t.cd_col = false;
+        t.vec_a = a.vec_a;  // ki is a multiple of 32: rows stay 16-byte aligned
+        t.vec_b = t.vec_c = t.vec_d = true;  // row-major B, C, D: element accesses
+        e = sgemm_emu::launch_gemm_acc(t, MFMAE_SHAPE_32x32x16, true, stream);
+        if (e != hipSuccess) return e;
+    }
+    if (in.n < a.n) {
+        sgemm_emu::GemmArgs r = a;
+        r.m = in.m;
+        r.n = a.n - in.n;
+        r.B = a.B + in.n;
+        r.C = a.C + in.n;
+        r.vec_b = a.vec_b && in.n % 4 == 0;
+        e = run_strip(r, stream);
+        if (e != hipSuccess) return e;
+    }
+    if (in.m < a.m) {
+        sgemm_emu::GemmArgs b = a;
+        b.m = a.m - in.m;
+        b.A = a.A + (int64_t)in.m * a.lda;
+        b.C = a.C + (int64_t)in.m * a.ldc;
+        e = run_strip(b, stream);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
              int ldc, int batch, sgemm_emu_stride_t st, int flow, int ec, int tile,
              hipStream_t stream) {
@@ -158,6 +265,7 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
     switch (kern) {
         case K_REG: e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream); break;
         case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, flow, stream); break;
+        case K_TILED: e = run_tiled(a, tile, stream); break;
         default: e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream); break;
     }
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);

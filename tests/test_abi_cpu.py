@@ -163,8 +163,22 @@ def test_resolve_policy():
     # ragged small products: register-direct 128x128
     assert _resolve(130, 132, 100, 8, (130 * 100, 100 * 132, 130 * 132)) == (
         0, (pkg.FLOW_REG, 1, pkg.TILE_128x128))
-    # not a multiple of any full tile and large: the general LDS kernel
-    assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    # large and ragged: whole tiles of the interior on the full-tile kernel,
+    # the edge strips on the register-flow kernel
+    assert _resolve(8192 - 64, 8192, 8192) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
+    assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
+    assert _resolve(8000, 8000, 8008) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))  # k tail 8
+    assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
+    # too little work to pay for the extra launches: the general LDS kernel
+    assert _resolve(2000, 2000, 32)[1][0] == pkg.FLOW_SPLIT
+    assert _resolve.kernel == "bgemm_emu_kernel"
+    assert _resolve(2100, 2300, 1000) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
+    # interior below 90% of C with every tile: the general LDS kernel
+    assert _resolve(1100, 1100, 512) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x128))
+    assert _resolve.kernel == "bgemm_emu_kernel"
+    # unaligned rows (k not a multiple of 4): the general LDS kernel
+    assert _resolve(4000, 4000, 4001)[1][0] == pkg.FLOW_SPLIT
     assert _resolve.kernel == "bgemm_emu_kernel"
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT

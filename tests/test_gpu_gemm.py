@@ -361,3 +361,41 @@ def test_workload_paper_sweep_k256_sampled():
         ref = oracle.dots(A[it].numpy()[rows], np.ascontiguousarray(B[it].numpy()[:, cols].T))
         gate(C[it][rows, cols], ref, w.k, f"paper_k256 item {it}")
 
+
+
+# Large ragged products: interior of whole tiles on the full-tile kernel, a
+# k tail added in place, edge strips on the register-flow kernel.
+TILED_SHAPES = [(1, 2100, 2300, 1000),   # 256 x 128 interior, k tail of 8, both strips
+                (2, 1500, 1800, 1024),   # 128 x 256 interior, whole k chunks, batch of 2
+                (3, 1200, 1300, 1000),   # 128 x 128 interior, batch of 3
+                (1, 2048, 2100, 1024),   # right strip only
+                (1, 2100, 2048, 1024)]   # bottom strip only
+
+
+@pytest.mark.parametrize("shape", TILED_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_tiled_ragged_large(shape):
+    batch, m, n, k = shape
+    print(f"case tiled {shape}", flush=True)
+    dev = device()
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=71 + m + k)
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.full((batch, m, n), float("nan"), device=dev)
+    pol, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, C)
+    assert kern == "bgemm_big_kernel+bgemm_reg_kernel", kern
+    pkg.sgemm_emu_batched(Ad, Bd, C)
+    Cn = to_np(C)
+    assert np.isfinite(Cn).all()
+    bm = 256 if pol.tile == pkg.TILE_256x128 else 128
+    bn = 256 if pol.tile == pkg.TILE_128x256 else 128
+    mi, ni = m - m % bm, n - n % bn
+    g = np.random.default_rng(m + n + k)
+    rows = np.unique(np.concatenate([[0, bm - 1, bm, mi - 1, min(mi, m - 1), m - 1],
+                                     g.integers(0, m, 10)]))
+    cols = np.unique(np.concatenate([[0, bn - 1, bn, ni - 1, min(ni, n - 1), n - 1],
+                                     g.integers(0, n, 10)]))
+    for b in range(batch):
+        rr, cc = np.meshgrid(rows, cols, indexing="ij")
+        rr, cc = rr.ravel(), cc.ravel()
+        An, Bn = A[b].numpy(), B[b].numpy()
+        ref = oracle.dots(An[rr], np.ascontiguousarray(Bn[:, cc].T))
+        gate(Cn[b][rr, cc], ref, k, f"tiled {shape} item {b}")
