@@ -1,24 +1,34 @@
 // Emulated SGEMM on full tiles of C (Sec. 4.4): split once per workgroup at
 // staging, hi/lo planes in LDS.
 //
-// Per k chunk of 32, every thread loads runs of 8 consecutive k of the
-// operands from global memory into registers (A: 8 consecutive floats of one
-// row; B: 8 rows of one column, one 256-byte row segment per wave and load),
-// splits them there and writes 16-byte hi and lo pieces to LDS, so each
-// element is split once per workgroup and LDS holds 2 + 2 bytes per element,
-// the footprint of the FP32 data.  Waves of 64 x 64 read their operand
-// vectors with one 16-byte LDS read per fragment and run 3 MFMAs per 32 x 32
-// block and 16-wide k step (v_mfma_f32_32x32x16_f16), main and correction
-// products in separate accumulators.
+// Per k chunk of 32, every thread loads its part of the chunk from global
+// memory into registers with 16-byte loads along the rows of A and of B (A:
+// 8 consecutive k of one row; B: 4 consecutive n of one k row, one 1 KiB row
+// per wave and load), splits the values there and writes hi and lo to LDS,
+// so each element is split once per workgroup and LDS holds 2 + 2 bytes per
+// element, the footprint of the FP32 data.  Waves of 64 x 64 build their
+// operand vectors from LDS and run 3 MFMAs per 32 x 32 block and 16-wide k
+// step (v_mfma_f32_32x32x16_f16), main and correction products in separate
+// accumulators.
 //
-// LDS layout: a plane (A hi, A lo, B hi, B lo) is [row][4 pieces of 8
-// halves], 64 bytes per row, no padding; piece q of row r is stored at
-// position q ^ ((r ^ (r >> 2)) & 3).  Measured on gfx950 (16-byte LDS
-// accesses, timed against a linear pattern), this swizzle makes all three
-// access patterns conflict-free: the fragment reads (lanes 0..31 rows
-// r..r+31 at one piece, lanes 32..63 the next piece), the A staging writes (4
-// lanes per row, one piece each) and the B staging writes (one row per lane,
-// one piece); unswizzled 64-byte rows give 4-way conflicts on the reads.
+// LDS layout, A planes (A hi, A lo): [row][4 pieces of 8 halves], 64 bytes
+// per row, no padding; piece q of row r is stored at position
+// q ^ ((r ^ (r >> 2)) & 3).  Measured on gfx950 (16-byte LDS accesses, timed
+// against a linear pattern), this swizzle makes the fragment reads (lanes
+// 0..31 rows r..r+31 at one piece, lanes 32..63 the next piece) and the
+// staging writes (4 lanes per row, one piece each) conflict-free.
+//
+// B planes (B hi, B lo): n-major, [k][BN halves], quad q (4 halves) of row k
+// at position q ^ (8 (k & 3)).  The MFMA wants 8 consecutive k of one column
+// per lane; gfx950's transposing LDS read (ds_read_b64_tr_b16) delivers them
+// from this layout, two 8-byte reads per fragment: in a group of 16 lanes,
+// lane 4i + c receives element c of the reads of lanes i, i + 4, i + 8 and
+// i + 12 of the group (lane layout checked on the device).  The swizzle puts
+// the 4 rows one half-wave reads (64 bytes each) and the 256-byte half-rows
+// the staging writes on distinct banks.  Loading B as whole rows instead of
+// 8 strided rows per lane cuts its vector-memory instructions by 4, which
+// was the binding limit of the k loop (measured: with half of those loads
+// the loop runs as fast as with none).
 //
 // Pipeline: two LDS stages and two register stages.  In iteration c the
 // workgroup computes chunk c, writes chunk c + 1 (loaded two iterations
@@ -90,6 +100,11 @@ struct BigCfg {
     static constexpr int A_UNITS = BM * (BK / 8) / NT;
     static constexpr int B_UNITS = BN * (BK / 8) / NT;
     static_assert(A_UNITS * NT == BM * (BK / 8) && B_UNITS * NT == BN * (BK / 8), "staging");
+    // split flow, B: quads of 4 consecutive n of one k row; one pass of the
+    // workgroup covers B_PASS_ROWS rows, each thread loads B_QUADS quads
+    static constexpr int B_QUADS = BK * BN / 4 / NT;
+    static constexpr int B_PASS_ROWS = NT / (BN / 4);
+    static_assert(B_QUADS * NT * 4 == BK * BN && B_PASS_ROWS % 4 == 0, "B quads");
     static_assert(WM % 32 == 0 && WN % 32 == 0, "blocks");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS of one CU");
 };
@@ -118,36 +133,91 @@ __device__ inline int piece32(int r, int p) {
     return r * 128 + 16 * (p ^ ((r ^ (r >> 3)) & 7));
 }
 
+// Byte offset of quad q (4 halves) of row k in an n-major B plane of BN
+// halves per row.  The swizzle flips bits 3 and 4 of q, so q stays in the
+// row (BN / 4 is a multiple of 32).
+template <class CF>
+__device__ inline int bquad(int k, int q) {
+    return k * (2 * CF::BN) + 8 * (q ^ (8 * (k & 3)));
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+
+// Transposing 8-byte LDS read (ds_read_b64_tr_b16).
+__device__ inline half4_t read_tr(const unsigned char* p) {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    return __builtin_bit_cast(half4_t,
+                              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p)));
+}
+
 // Registers of one staged chunk.
 template <class CF>
 struct Stage {
     f32x4 a[CF::A_UNITS][2];
-    float b[CF::B_UNITS][8];
+    f32x4 bq[CF::B_QUADS];    // split flow
+    float b[CF::B_UNITS][8];  // FP32 flows
 };
 
-// Per-thread staging coordinates (constant over the k loop).
+// Per-thread staging coordinates.  The task's corner addresses are the same
+// for the whole workgroup (scalar registers); each thread adds a 32-bit byte
+// offset.  The loads are buffer loads on a descriptor made from the chunk's
+// corner (scalar), the thread's offset (vector) and the row's offset
+// (scalar), so no load needs 64-bit address arithmetic on the VALU.
 template <class CF>
 struct StageMap {
-    const float* a[CF::A_UNITS];  // A[m0 + row][8 q]
-    const float* b[CF::B_UNITS];  // B[8 kg][n0 + n]
+    const float* a;               // A[m0][0] of the task
+    const float* b;               // B[0][n0] of the task
     int64_t ldb;
+    uint32_t a_off[CF::A_UNITS];  // bytes from a to A[m0 + row][8 q]
+    uint32_t b_off[CF::B_UNITS];  // FP32 flows: bytes from b to B[8 kg][n0 + n]
+    uint32_t bq_off;              // split flow: bytes from b to B[row][n0 + 4 q]
     int a_lds[CF::A_UNITS];       // piece(row, q), or piece32(row, 2q) for FP32 stages
-    int b_lds[CF::B_UNITS];       // piece(n, kg), or piece32(n, 2kg)
+    int b_lds[CF::B_UNITS];       // FP32 flows: piece32(n, 2kg)
+    int bq_lds;                   // split flow: bquad(row, q)
 };
+
+// Raw buffer descriptor on p: byte offsets up to 2^32 - 1, no stride, 32-bit
+// data format (the fourth word as for every gfx9 raw buffer).
+__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const float* p) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), 0, -1, 0x00020000);
+}
 
 template <class CF>
 __device__ inline void load_stage(Stage<CF>& st, const StageMap<CF>& sm, int k0) {
+    const __amdgpu_buffer_rsrc_t ra = raw_rsrc(sm.a + k0);
 #pragma unroll
     for (int u = 0; u < CF::A_UNITS; ++u) {
-        st.a[u][0] = *reinterpret_cast<const f32x4*>(sm.a[u] + k0);
-        st.a[u][1] = *reinterpret_cast<const f32x4*>(sm.a[u] + k0 + 4);
+        st.a[u][0] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, sm.a_off[u], 0, 0));
+        st.a[u][1] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, sm.a_off[u] + 16, 0, 0));
     }
+    const __amdgpu_buffer_rsrc_t rb = raw_rsrc(sm.b + (int64_t)k0 * sm.ldb);
+    const uint32_t row = (uint32_t)sm.ldb * 4u;  // bytes; a chunk fits in 32 bits (offsets_fit)
+    if constexpr (CF::FLOW == BIG_SPLIT) {
 #pragma unroll
-    for (int u = 0; u < CF::B_UNITS; ++u) {
-        const float* bp = sm.b[u] + (int64_t)k0 * sm.ldb;
+        for (int r = 0; r < CF::B_QUADS; ++r)
+            st.bq[r] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                           rb, sm.bq_off, (int)(row * (uint32_t)(r * CF::B_PASS_ROWS)), 0));
+    } else {
 #pragma unroll
-        for (int v = 0; v < 8; ++v) st.b[u][v] = bp[(int64_t)v * sm.ldb];
+        for (int v = 0; v < 8; ++v)
+#pragma unroll
+            for (int u = 0; u < CF::B_UNITS; ++u)
+                st.b[u][v] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(rb, sm.b_off[u],
+                                                                (int)(row * (uint32_t)v), 0));
     }
+}
+
+// The byte offsets of StageMap fit in 32 bits.
+template <class CF>
+bool offsets_fit(const GemmArgs& a) {
+    const int64_t lim = (int64_t)1 << 32;
+    return ((int64_t)CF::BM * a.lda + CF::BK) * 4 < lim &&
+           ((int64_t)CF::BK * a.ldb + CF::BN) * 4 < lim;
 }
 
 // Write the staged chunk to LDS stage `buf`: split into hi and lo pieces
@@ -186,11 +256,13 @@ __device__ inline void store_stage(const Stage<CF>& st, const StageMap<CF>& sm,
         *reinterpret_cast<half8_t*>(a_lo + sm.a_lds[u]) = lo;
     }
 #pragma unroll
-    for (int u = 0; u < CF::B_UNITS; ++u) {
-        half8_t hi, lo;
-        mfmae::tcec::split8(st.b[u], hi, lo);
-        *reinterpret_cast<half8_t*>(b_hi + sm.b_lds[u]) = hi;
-        *reinterpret_cast<half8_t*>(b_lo + sm.b_lds[u]) = lo;
+    for (int r = 0; r < CF::B_QUADS; ++r) {
+        mfmae::tcec::half2_t h0, l0, h1, l1;
+        mfmae::tcec::split_pair(st.bq[r][0], st.bq[r][1], h0, l0);
+        mfmae::tcec::split_pair(st.bq[r][2], st.bq[r][3], h1, l1);
+        const int o = sm.bq_lds + r * CF::B_PASS_ROWS * 2 * CF::BN;
+        *reinterpret_cast<half4_t*>(b_hi + o) = half4_t{h0[0], h0[1], h1[0], h1[1]};
+        *reinterpret_cast<half4_t*>(b_lo + o) = half4_t{l0[0], l0[1], l1[0], l1[1]};
     }
 }
 
@@ -281,11 +353,31 @@ __device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
                 ahi[tm] = *reinterpret_cast<const half8_t*>(a_hi + o);
                 alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
             }
+            if constexpr (CF::FLOW == BIG_SPLIT) {
+                // lane 16 G + sl reads row 8 (G / 2) + sl / 4 (+ 4 for the
+                // second half of the 8 k) at quad 4 (G % 2) + sl % 4 of the
+                // block; the transpose hands lane (j, g) rows 16 s + 8 g + 0..7
+                // of column j
+                const int l = threadIdx.x & 63;
+                const int sl = l & 15, G = l >> 4;
+                const int kl = 16 * s + 8 * (G >> 1) + (sl >> 2);
+                const int ql = 4 * (G & 1) + (sl & 3);
 #pragma unroll
-            for (int tn = 0; tn < CF::TN; ++tn) {
-                const int o = piece(brow + 32 * tn + j, q);
-                bhi[tn] = *reinterpret_cast<const half8_t*>(b_hi + o);
-                blo[tn] = *reinterpret_cast<const half8_t*>(b_lo + o);
+                for (int tn = 0; tn < CF::TN; ++tn) {
+                    const int o = bquad<CF>(kl, 8 * ((brow >> 5) + tn) + ql);
+                    const int o4 = o + 4 * 2 * CF::BN;  // rows + 4: same swizzle
+                    const half4_t h0 = read_tr(b_hi + o), h1 = read_tr(b_hi + o4);
+                    const half4_t l0 = read_tr(b_lo + o), l1 = read_tr(b_lo + o4);
+                    bhi[tn] = half8_t{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+                    blo[tn] = half8_t{l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+                }
+            } else {
+#pragma unroll
+                for (int tn = 0; tn < CF::TN; ++tn) {
+                    const int o = piece(brow + 32 * tn + j, q);
+                    bhi[tn] = *reinterpret_cast<const half8_t*>(b_hi + o);
+                    blo[tn] = *reinterpret_cast<const half8_t*>(b_lo + o);
+                }
             }
         }
 #pragma unroll
@@ -357,21 +449,28 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
 
     const int tid = threadIdx.x;
     StageMap<CF> sm;
+    sm.a = Ab + (int64_t)m0 * p.lda;
+    sm.b = Bb + n0;
+    sm.ldb = p.ldb;
 #pragma unroll
     for (int u = 0; u < CF::A_UNITS; ++u) {
         const int unit = u * CF::NT + tid;
         const int row = unit >> 2, q = unit & 3;
-        sm.a[u] = Ab + (int64_t)(m0 + row) * p.lda + 8 * q;
+        sm.a_off[u] = (uint32_t)(row * p.lda + 8 * q) * 4u;
         sm.a_lds[u] = CF::FLOW == BIG_SPLIT ? piece(row, q) : piece32(row, 2 * q);
     }
 #pragma unroll
     for (int u = 0; u < CF::B_UNITS; ++u) {
         const int unit = u * CF::NT + tid;
         const int n = unit % CF::BN, kg = unit / CF::BN;
-        sm.b[u] = Bb + (int64_t)(8 * kg) * p.ldb + n0 + n;
-        sm.b_lds[u] = CF::FLOW == BIG_SPLIT ? piece(n, kg) : piece32(n, 2 * kg);
+        sm.b_off[u] = (uint32_t)(8 * kg * p.ldb + n) * 4u;
+        sm.b_lds[u] = piece32(n, 2 * kg);
     }
-    sm.ldb = p.ldb;
+    {
+        const int q = tid % (CF::BN / 4), row = tid / (CF::BN / 4);
+        sm.bq_off = (uint32_t)(row * p.ldb + 4 * q) * 4u;
+        sm.bq_lds = bquad<CF>(row, q);
+    }
 
     const int wave = tid >> 6;
     const int l = tid & 63;
@@ -468,36 +567,33 @@ __device__ inline TaskGeo task_geo(const BigParams& p, int task) {
 // Global addresses of this thread's staging units for task geometry q.
 template <class CF>
 __device__ inline void map_task(StageMap<CF>& sm, const BigParams& p, const TaskGeo& q) {
-    const int tid = threadIdx.x;
-#pragma unroll
-    for (int u = 0; u < CF::A_UNITS; ++u) {
-        const int unit = u * CF::NT + tid;
-        const int row = unit >> 2, qq = unit & 3;
-        sm.a[u] = q.A + (int64_t)(q.m0 + row) * p.lda + 8 * qq;
-    }
-#pragma unroll
-    for (int u = 0; u < CF::B_UNITS; ++u) {
-        const int unit = u * CF::NT + tid;
-        const int n = unit % CF::BN, kg = unit / CF::BN;
-        sm.b[u] = q.B + (int64_t)(8 * kg) * p.ldb + q.n0 + n;
-    }
+    sm.a = q.A + (int64_t)q.m0 * p.lda;
+    sm.b = q.B + q.n0;
 }
 
-// LDS offsets of this thread's staging units (the same for every task).
+// Byte offsets and LDS offsets of this thread's staging units (the same for
+// every task).
 template <class CF>
-__device__ inline void map_lds(StageMap<CF>& sm) {
+__device__ inline void map_lds(StageMap<CF>& sm, const BigParams& p) {
     const int tid = threadIdx.x;
 #pragma unroll
     for (int u = 0; u < CF::A_UNITS; ++u) {
         const int unit = u * CF::NT + tid;
         const int row = unit >> 2, q = unit & 3;
+        sm.a_off[u] = (uint32_t)(row * p.lda + 8 * q) * 4u;
         sm.a_lds[u] = CF::FLOW == BIG_SPLIT ? piece(row, q) : piece32(row, 2 * q);
     }
 #pragma unroll
     for (int u = 0; u < CF::B_UNITS; ++u) {
         const int unit = u * CF::NT + tid;
         const int n = unit % CF::BN, kg = unit / CF::BN;
-        sm.b_lds[u] = CF::FLOW == BIG_SPLIT ? piece(n, kg) : piece32(n, 2 * kg);
+        sm.b_off[u] = (uint32_t)(8 * kg * p.ldb + n) * 4u;
+        sm.b_lds[u] = piece32(n, 2 * kg);
+    }
+    {
+        const int q = tid % (CF::BN / 4), row = tid / (CF::BN / 4);
+        sm.bq_off = (uint32_t)(row * p.ldb + 4 * q) * 4u;
+        sm.bq_lds = bquad<CF>(row, q);
     }
 }
 
@@ -548,7 +644,7 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_stream_kernel(BigPara
     const int wcol = (wave % CF::WAVES_N) * CF::WN;
 
     StageMap<CF> sm;
-    map_lds<CF>(sm);
+    map_lds<CF>(sm, p);
     sm.ldb = p.ldb;
     map_task<CF>(sm, p, task_geo<CF>(p, t0));
     // load cursor: task index li of this workgroup, chunk lc.  Past the end
@@ -717,7 +813,7 @@ using Big128x128Staged = BigCfg<128, 128, 2, 2, 2, 0, BIG_STAGED>;
 template <class CF>
 bool fits(const GemmArgs& a) {
     return a.m % CF::BM == 0 && a.n % CF::BN == 0 && a.k % CF::BK == 0 && a.k > 0 && a.vec_a &&
-           a.vec_b;
+           a.vec_b && offsets_fit<CF>(a);
 }
 
 }  // namespace
