@@ -47,10 +47,36 @@ struct Block {
     float x[2][8];
 };
 
-// Whole block inside a 16-byte aligned row: four 16-byte loads.
-__device__ inline void load_fast(Block& b, const float* row, int c0) {
+// A block as loaded on the whole-block path: lane l holds values
+// 256 i + 4 l .. + 3, i = 0..3, so every load instruction reads 1 KiB of
+// whole cache lines.
+struct Raw {
+    f32x4 v[4];
+};
+
+// Whole block inside a 16-byte aligned row: four contiguous 16-byte loads.
+__device__ inline void load_fast(Raw& b, const float* row, int c0) {
     const int l = threadIdx.x & 63;
-    const float* q = row + c0 + 32 * (l & 31) + 8 * (l >> 5);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) b.v[i] = *reinterpret_cast<const f32x4*>(row + c0 + 256 * i + 4 * l);
+}
+
+// The wave's LDS copy of one block: segment n (32 values) at 36 n floats.
+// With this pitch the 16-byte accesses of the operand and accumulator
+// layouts (lanes n = 0..15 at 36 n + c) fall on distinct banks.
+constexpr int kSegPitch = 36;
+constexpr int kStageFloats = 32 * kSegPitch;
+
+__device__ inline int staged(int value) { return kSegPitch * (value >> 5) + (value & 31); }
+
+// Regroup a contiguous block into the operand layout through the wave's
+// LDS buffer (other lanes' values: ordered by the wave fence).
+__device__ inline void to_operand(const Raw& r, float* buf, Block& b) {
+    const int l = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<f32x4*>(buf + staged(256 * i + 4 * l)) = r.v[i];
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+    const float* q = buf + kSegPitch * (l & 31) + 8 * (l >> 5);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         const f32x4 v0 = *reinterpret_cast<const f32x4*>(q + 16 * s);
@@ -115,13 +141,21 @@ __device__ inline void scan_block(const Block& b, const half8_t (&Ut)[2], float&
     carry = carry + __shfl(incl, 31, 64);
 }
 
-__device__ inline void store_fast(float* row, int c0, const float (&y)[16]) {
+// Outputs in the accumulator layout, regrouped through the wave's LDS
+// buffer and stored as four contiguous 1 KiB instructions.
+__device__ inline void store_fast(float* row, int c0, const float (&y)[16], float* buf) {
     const int l = threadIdx.x & 63;
-    float* q = row + c0 + 32 * (l & 31) + 4 * (l >> 5);
+    float* q = buf + kSegPitch * (l & 31) + 4 * (l >> 5);
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");  // operand reads done
 #pragma unroll
     for (int g = 0; g < 4; ++g)
         *reinterpret_cast<f32x4*>(q + 8 * g) = f32x4{y[4 * g], y[4 * g + 1], y[4 * g + 2],
                                                      y[4 * g + 3]};
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<f32x4*>(row + c0 + 256 * i + 4 * l) =
+            *reinterpret_cast<const f32x4*>(buf + staged(256 * i + 4 * l));
 }
 
 __device__ inline void store_bounded(float* row, int c0, int len, const float (&y)[16]) {
@@ -135,6 +169,7 @@ __device__ inline void store_bounded(float* row, int c0, int len, const float (&
 }
 
 __global__ __launch_bounds__(64 * kWaves, 2) void scan_kernel(ScanArgs p) {
+    __shared__ __attribute__((aligned(16))) float stage[kWaves][kStageFloats];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t r_first = ((int64_t)blockIdx.x * kWaves + wave) * kRowsPerWave;
     if (r_first >= p.rows) return;  // whole wave; no barrier below
@@ -165,20 +200,23 @@ __global__ __launch_bounds__(64 * kWaves, 2) void scan_kernel(ScanArgs p) {
         const int last = nf - 1;
         auto row_in = [&](int f) { return p.X + (r_first + f / nb) * p.ldx; };
         auto row_out = [&](int f) { return p.Y + (r_first + f / nb) * p.ldy; };
-        auto load = [&](Block& b, int f) {
+        float* sb = stage[wave];
+        auto load = [&](Raw& b, int f) {
             const int fc = min(f, last);
             load_fast(b, row_in(fc), 1024 * (fc % nb));
         };
         // the scheduling barrier keeps each step's reload in place, so the
         // blocks really are loaded kBuf steps ahead
-        auto step = [&](Block& b, int f) {
+        auto step = [&](Raw& r, int f) {
             if (f % nb == 0) carry = 0.0f;
+            Block b;
+            to_operand(r, sb, b);
             scan_block(b, Ut, carry, y);
-            store_fast(row_out(f), 1024 * (f % nb), y);
-            load(b, f + kBuf);
+            store_fast(row_out(f), 1024 * (f % nb), y, sb);
+            load(r, f + kBuf);
             __builtin_amdgcn_sched_barrier(0);
         };
-        Block buf[kBuf];
+        Raw buf[kBuf];
 #pragma unroll
         for (int i = 0; i < kBuf; ++i) load(buf[i], i);
         int f = 0;
@@ -195,8 +233,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void scan_kernel(ScanArgs p) {
         for (int i = 0; i < kBuf - 1; ++i) {
             if (f + i < nf) {
                 if ((f + i) % nb == 0) carry = 0.0f;
-                scan_block(buf[i], Ut, carry, y);
-                store_fast(row_out(f + i), 1024 * ((f + i) % nb), y);
+                Block b;
+                to_operand(buf[i], sb, b);
+                scan_block(b, Ut, carry, y);
+                store_fast(row_out(f + i), 1024 * ((f + i) % nb), y, sb);
             }
         }
         return;
