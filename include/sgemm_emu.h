@@ -84,19 +84,22 @@ int sgemm_emu_batched(int m, int n, int k,
  *                         full-tile kernel applies (see
  *                         sgemm_emu_resolve_policy): 128x256 when k >= 1024
  *                         and batch * m * n >= 2048 * 2048, else 256x128,
- *                         else 128x128; otherwise REG for products up to
- *                         1024 x 1024 whose operands allow its vector loads;
- *                         otherwise, for m and n above 1024 with 16-byte
- *                         aligned A and B rows, k >= 32 and at least 2^32
- *                         multiply-adds (batch m n k), the largest of
- *                         those tiles whose whole tiles cover at least 90%
- *                         of C: that interior (and k rounded down to a
- *                         multiple of 32) runs on the full-tile kernel, the
+ *                         else 128x128.  Otherwise, for m and n above 1024
+ *                         with 16-byte aligned A and B rows, k >= 32, at
+ *                         least 2^35 multiply-adds (batch m n k) and the
+ *                         REG flow's conditions met, the first of 128x256
+ *                         (when it is preferred as above) and 256x128 whose
+ *                         whole tiles cover at least 95% of C and number at
+ *                         least 256 (batch included):
+ *                         that interior (and k rounded down to a multiple
+ *                         of 32) runs on the full-tile kernel, the
  *                         remaining k is added to it in place, and the edge
- *                         strips run on the REG flow with 64 x 64 tiles
- *                         (when A and the leading dimensions allow it), one
- *                         launch after another on the stream; otherwise
- *                         SPLIT.
+ *                         strips run on the REG flow with 64 x 64 tiles, one
+ *                         launch after another on the stream.  Otherwise
+ *                         REG whenever its conditions hold: tile 64x64 for
+ *                         m, n <= 64, else 128x128, else (B rows without
+ *                         vector loads, below 2^35 multiply-adds) 64x64.
+ *                         Otherwise SPLIT on the general kernel.
  *   SGEMM_EMU_FLOW_SPLIT  FP32 tiles are split in registers between the
  *                         global load and the LDS store; LDS holds hi and lo
  *                         (the same 4 bytes per element as FP32) and the

@@ -121,54 +121,74 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     a.vec_a = aligned16(A) && lda % 4 == 0 && st.a % 4 == 0;
     a.vec_b = aligned16(B) && ldb % 4 == 0 && st.b % 4 == 0;
     if (flow == SGEMM_EMU_FLOW_AUTO) {
-        // Full 256 x 128 tiles take the pipelined split-flow kernel (each
-        // element split once per workgroup).  Other small products are
-        // bound by HBM traffic: the barrier-free register-direct flow keeps
-        // the most bytes in flight.  Large ragged ones need the LDS-shared
-        // tiles to stay off the L2 bandwidth limit.
-        const int reg_tile = (m <= 64 && n <= 64) ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
+        // Full tiles take the pipelined split-flow kernel (each element
+        // split once per workgroup).  Other products take the barrier-free
+        // register-direct flow, which keeps the most bytes in flight: 1.8-5x
+        // the general LDS kernel's rate on every shape measured (1100 x 1500
+        // x 2000: 76 against 397 us; 8000^3: 5.9 against 7.2 ms).  From
+        // 2^35 multiply-adds on, a large ragged product whose whole tiles
+        // cover nearly all of C runs faster decomposed: those tiles on the
+        // full-tile kernel, the rest on the accumulate and register-flow
+        // kernels (4000^3: 557 against 613 us; 8000^3: 3.5 against 5.9 ms;
+        // 3000^3: 338 against 320 us).  The general kernel is left for
+        // unaligned operands.
         int big_tile = SGEMM_EMU_TILE_AUTO;
+        const bool wide = k >= 1024 && (int64_t)m * n * batch >= (int64_t)2048 * 2048;
+        // 128x256 pays off for long k loops over much output (measured on
+        // 8192^3 and on 256 x 1024 x 1024 x k for k >= 1024)
+        const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
+                              SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
         if (ec == 1) {
-            // 128x256 pays off for long k loops over much output (measured on
-            // 8192^3 and on 256 x 1024 x 1024 x k for k >= 1024)
-            const bool wide = k >= 1024 && (int64_t)m * n * batch >= (int64_t)2048 * 2048;
-            const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
-                                  SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
             for (int t : order)
                 if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&
                     sgemm_emu::big_supported(a, t, SGEMM_EMU_FLOW_SPLIT))
                     big_tile = t;
         }
+        const double work = (double)batch * m * n * k;  // multiply-adds (no overflow)
+        const double kDecompose = 34359738368.0;         // 2^35
+        // the decomposition: whole tiles covering at least 95% of C, at least
+        // one per CU (measured: 0.95-0.98 coverage won or tied, 0.92-0.94 lost
+        // to the register-direct flow by 1.2-1.4x)
+        int tiled = SGEMM_EMU_TILE_AUTO;
+        if (big_tile == SGEMM_EMU_TILE_AUTO && ec == 1 && tile == SGEMM_EMU_TILE_AUTO &&
+            a.vec_a && a.vec_b && m > 1024 && n > 1024 && k >= 32 &&
+            work >= kDecompose && sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_64x64)) {
+            // (the 128 x 128 interior lost on every shape measured)
+            for (int t : {order[0], order[1]}) {
+                const Interior in = interior(a, t);
+                const int64_t ntiles =
+                    (int64_t)(in.m / tile_rows(t)) * (in.n / tile_cols(t)) * batch;
+                if (tiled == SGEMM_EMU_TILE_AUTO && ntiles >= 256 &&
+                    (int64_t)in.m * in.n * 20 >= (int64_t)m * n * 19)
+                    tiled = t;
+            }
+        }
+        // register-direct tile: 64x64 for products inside one such tile or
+        // B rows that allow no vector loads (that one only below 2^35
+        // multiply-adds: measured only there), else 128x128
+        int reg_tile = SGEMM_EMU_TILE_AUTO;
+        if (m <= 64 && n <= 64) {
+            if (sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_64x64))
+                reg_tile = SGEMM_EMU_TILE_64x64;
+        } else if (sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_128x128)) {
+            reg_tile = SGEMM_EMU_TILE_128x128;
+        } else if (work < kDecompose && sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_64x64)) {
+            reg_tile = SGEMM_EMU_TILE_64x64;
+        }
+        if (tile != SGEMM_EMU_TILE_AUTO && tile != reg_tile) reg_tile = SGEMM_EMU_TILE_AUTO;
         if (big_tile != SGEMM_EMU_TILE_AUTO) {
             flow = SGEMM_EMU_FLOW_SPLIT;
             tile = big_tile;
-        } else if (m <= 1024 && n <= 1024 && (tile == SGEMM_EMU_TILE_AUTO || tile == reg_tile) &&
-                   sgemm_emu::reg_flow_supported(a, reg_tile)) {
+        } else if (tiled != SGEMM_EMU_TILE_AUTO) {
+            flow = SGEMM_EMU_FLOW_SPLIT;
+            tile = tiled;
+            kern = K_TILED;
+            return SGEMM_EMU_OK;
+        } else if (reg_tile != SGEMM_EMU_TILE_AUTO) {
             flow = SGEMM_EMU_FLOW_REG;
             tile = reg_tile;
         } else {
             flow = SGEMM_EMU_FLOW_SPLIT;
-            // Large ragged products: whole tiles covering at least 90% of C
-            // run on the full-tile kernel, the k tail on the accumulate
-            // kernel and the edge strips on the register-flow kernel (1.9x
-            // the general kernel's rate on 8000^3 and 6000^3, 1.6x on 2100 x
-            // 2300 x 1000).  Below 2^32 multiply-adds the extra launches
-            // cost more than they gain (measured on 2 x 1500 x 1800 x 544).
-            if (ec == 1 && tile == SGEMM_EMU_TILE_AUTO && a.vec_a && a.vec_b && m > 1024 &&
-                n > 1024 && k >= 32 && (int64_t)batch * m * n * k >= ((int64_t)1 << 32) &&
-                sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_64x64)) {
-                const bool wide = k >= 1024 && (int64_t)m * n * batch >= (int64_t)2048 * 2048;
-                const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
-                                      SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
-                for (int t : order) {
-                    const Interior in = interior(a, t);
-                    if ((int64_t)in.m * in.n * 10 >= (int64_t)m * n * 9) {
-                        tile = t;
-                        kern = K_TILED;
-                        return SGEMM_EMU_OK;
-                    }
-                }
-            }
         }
     }
     if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);

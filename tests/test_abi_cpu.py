@@ -169,13 +169,21 @@ def test_resolve_policy():
     assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
     assert _resolve(8000, 8000, 8008) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))  # k tail 8
     assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
-    # too little work to pay for the extra launches: the general LDS kernel
-    assert _resolve(2000, 2000, 32)[1][0] == pkg.FLOW_SPLIT
-    assert _resolve.kernel == "bgemm_emu_kernel"
-    assert _resolve(2100, 2300, 1000) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve(4100, 4300, 2060) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
     assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
-    # interior below 90% of C with every tile: the general LDS kernel
-    assert _resolve(1100, 1100, 512) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x128))
+    assert _resolve(6000, 6000, 960) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+    assert _resolve.kernel == "bgemm_big_kernel+bgemm_reg_kernel"
+    # ragged products below 2^35 multiply-adds, or whose whole tiles cover
+    # less than 95% of C: the register-direct flow
+    for shape in ((2000, 2000, 32), (2100, 2300, 1000), (1100, 1100, 512), (3000, 3000, 3000),
+                  (1100, 9000, 4000), (3300, 3500, 3000), (2300, 2200, 7000), (2700, 2700, 4740)):
+        assert _resolve(*shape) == (0, (pkg.FLOW_REG, 1, pkg.TILE_128x128)), shape
+        assert _resolve.kernel == "bgemm_reg_kernel"
+    # B rows without 8-byte vectors (n odd): 64 x 64 register tiles below
+    # 2^35 multiply-adds, the general kernel above
+    assert _resolve(1100, 1101, 512) == (0, (pkg.FLOW_REG, 1, pkg.TILE_64x64))
+    assert _resolve.kernel == "bgemm_reg_kernel"
+    assert _resolve(4000, 4001, 4000)[1][0] == pkg.FLOW_SPLIT
     assert _resolve.kernel == "bgemm_emu_kernel"
     # unaligned rows (k not a multiple of 4): the general LDS kernel
     assert _resolve(4000, 4000, 4001)[1][0] == pkg.FLOW_SPLIT

@@ -365,37 +365,55 @@ def test_workload_paper_sweep_k256_sampled():
 
 # Large ragged products: interior of whole tiles on the full-tile kernel, a
 # k tail added in place, edge strips on the register-flow kernel.
-TILED_SHAPES = [(1, 2100, 2300, 1000),   # 256 x 128 interior, k tail of 8, both strips
-                (2, 1500, 1800, 1024),   # 128 x 256 interior, whole k chunks, batch of 2
-                (3, 1200, 1300, 1000),   # 128 x 128 interior, batch of 3
-                (1, 2048, 2100, 1024),   # right strip only
-                (1, 2100, 2048, 1024)]   # bottom strip only
+TILED_SHAPES = [(1, 4100, 4300, 2060),   # 128 x 256 interior, k tail of 12, both strips
+                (2, 2600, 2600, 2560),   # whole k chunks, batch of 2
+                (1, 6000, 6000, 960),    # 256 x 128 interior
+                (1, 4096, 4200, 2048),   # right strip only
+                (1, 4200, 4096, 2048)]   # bottom strip only
+# Ragged products on the register-direct flow (below 2^35 multiply-adds or
+# without a nearly full interior): many tiles and long k; n odd takes the
+# 64 x 64 tiles.
+REG_SHAPES = [(1, 2100, 2300, 1000), (2, 1500, 1800, 1024), (3, 1200, 1300, 1000),
+              (1, 3300, 3500, 3000), (1, 1100, 1101, 512)]
 
 
-@pytest.mark.parametrize("shape", TILED_SHAPES, ids=lambda s: "x".join(map(str, s)))
-def test_tiled_ragged_large(shape):
+def _seams(m, n, bm, bn, seed):
+    mi, ni = m - m % bm, n - n % bn
+    g = np.random.default_rng(seed)
+    rows = np.unique(np.concatenate([[0, bm - 1, bm, mi - 1, min(mi, m - 1), m - 1],
+                                     g.integers(0, m, 10)]))
+    cols = np.unique(np.concatenate([[0, bn - 1, bn, ni - 1, min(ni, n - 1), n - 1],
+                                     g.integers(0, n, 10)]))
+    rr, cc = np.meshgrid(rows, cols, indexing="ij")
+    return rr.ravel(), cc.ravel()
+
+
+def _check_sampled(shape, expect_kernel, label):
     batch, m, n, k = shape
-    print(f"case tiled {shape}", flush=True)
+    print(f"case {label} {shape}", flush=True)
     dev = device()
     A, B = synth.gemm_inputs(batch, m, n, k, seed=71 + m + k)
     Ad, Bd = A.to(dev), B.to(dev)
     C = torch.full((batch, m, n), float("nan"), device=dev)
     pol, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, C)
-    assert kern == "bgemm_big_kernel+bgemm_reg_kernel", kern
+    assert kern == expect_kernel, kern
     pkg.sgemm_emu_batched(Ad, Bd, C)
-    Cn = to_np(C)
-    assert np.isfinite(Cn).all()
-    bm = 256 if pol.tile == pkg.TILE_256x128 else 128
-    bn = 256 if pol.tile == pkg.TILE_128x256 else 128
-    mi, ni = m - m % bm, n - n % bn
-    g = np.random.default_rng(m + n + k)
-    rows = np.unique(np.concatenate([[0, bm - 1, bm, mi - 1, min(mi, m - 1), m - 1],
-                                     g.integers(0, m, 10)]))
-    cols = np.unique(np.concatenate([[0, bn - 1, bn, ni - 1, min(ni, n - 1), n - 1],
-                                     g.integers(0, n, 10)]))
+    bm = 256 if pol.tile == pkg.TILE_256x128 else 64 if pol.tile == pkg.TILE_64x64 else 128
+    bn = 256 if pol.tile == pkg.TILE_128x256 else 64 if pol.tile == pkg.TILE_64x64 else 128
+    rr, cc = _seams(m, n, bm, bn, m + n + k)
     for b in range(batch):
-        rr, cc = np.meshgrid(rows, cols, indexing="ij")
-        rr, cc = rr.ravel(), cc.ravel()
+        Cb = C[b].cpu().numpy()
+        assert np.isfinite(Cb).all()
         An, Bn = A[b].numpy(), B[b].numpy()
         ref = oracle.dots(An[rr], np.ascontiguousarray(Bn[:, cc].T))
-        gate(Cn[b][rr, cc], ref, k, f"tiled {shape} item {b}")
+        gate(Cb[rr, cc], ref, k, f"{label} {shape} item {b}")
+
+
+@pytest.mark.parametrize("shape", TILED_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_tiled_ragged_large(shape):
+    _check_sampled(shape, "bgemm_big_kernel+bgemm_reg_kernel", "tiled")
+
+
+@pytest.mark.parametrize("shape", REG_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_register_flow_ragged_large(shape):
+    _check_sampled(shape, "bgemm_reg_kernel", "register flow")
