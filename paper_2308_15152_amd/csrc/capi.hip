@@ -64,11 +64,9 @@ int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int
     return SGEMM_EMU_OK;
 }
 
-// Validate, then resolve the policy (flow and tile, AUTO replaced by the
-// library's choice) and fill the kernel arguments.  `launch` is false for an
-// empty problem (nothing to run).
-// K_TILED: a large product whose shape does not fill whole tiles, run as
-// its interior of whole tiles on the full-tile kernel, a k tail (k mod 32
+// The kernels a GEMM call can run.  K_NONE: an empty problem (nothing to
+// run).  K_TILED: a large product whose shape does not fill whole tiles, run
+// as its interior of whole tiles on the full-tile kernel, a k tail (k mod 32
 // values) added in place by the accumulate kernel, and the edge strips on
 // the register-flow kernel.
 enum Kernel { K_NONE, K_REG, K_BIG, K_LDS, K_TILED };
@@ -95,6 +93,8 @@ Interior interior(const sgemm_emu::GemmArgs& a, int tile) {
     return {a.m - a.m % tile_rows(tile), a.n - a.n % tile_cols(tile), a.k - a.k % 32};
 }
 
+// Validate, then resolve the policy (flow and tile, AUTO replaced by the
+// library's choice), fill the kernel arguments and name the kernel.
 int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, int ldb, float* C,
                  int ldc, int batch, sgemm_emu_stride_t st, int& flow, int ec, int& tile,
                  sgemm_emu::GemmArgs& a, Kernel& kern) {
@@ -205,12 +205,6 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     return SGEMM_EMU_OK;
 }
 
-// K_TILED, in stream order: the interior C[0:mi, 0:ni] = A[0:mi, 0:ki]
-// B[0:ki, 0:ni] on the full-tile kernel; the k tail C[0:mi, 0:ni] +=
-// A[0:mi, ki:k] B[ki:k, 0:ni] in place; the right strip C[0:mi, ni:n] and
-// the bottom strip C[mi:m, 0:n] over the whole k on the register-flow
-// kernel (64 x 64 tiles).
-// Every piece is a view of the same operands (same ld and item strides).
 // An edge strip (at most one tile deep, long k): the barrier-free register
 // flow on 64 x 64 tiles runs 4-6x faster than the LDS-tiled general kernel
 // there (measured on 7936 x 64 x 8000 and 64 x 8000 x 8000), since the
@@ -221,6 +215,12 @@ hipError_t run_strip(const sgemm_emu::GemmArgs& s, hipStream_t stream) {
     return sgemm_emu::launch_gemm_reg(s, SGEMM_EMU_TILE_64x64, true, stream);
 }
 
+// K_TILED, in stream order: the interior C[0:mi, 0:ni] = A[0:mi, 0:ki]
+// B[0:ki, 0:ni] on the full-tile kernel; the k tail C[0:mi, 0:ni] +=
+// A[0:mi, ki:k] B[ki:k, 0:ni] in place; the right strip C[0:mi, ni:n] and
+// the bottom strip C[mi:m, 0:n] over the whole k on the register-flow
+// kernel (64 x 64 tiles).  Every piece is a view of the same operands (same
+// ld and item strides).
 hipError_t run_tiled(const sgemm_emu::GemmArgs& a, int tile, hipStream_t stream) {
     const Interior in = interior(a, tile);
     sgemm_emu::GemmArgs g = a;
@@ -249,7 +249,10 @@ hipError_t run_tiled(const sgemm_emu::GemmArgs& a, int tile, hipStream_t stream)
         t.batch = a.batch;
         t.a_trans = t.b_trans = t.cd_col = false;
         t.vec_a = a.vec_a;  // ki is a multiple of 32: rows stay 16-byte aligned
-        t.vec_b = t.vec_c = t.vec_d = true;  // row-major B, C, D: element accesses
+        // row-major B (k x n) and row-major C, D: the fragment loads and
+        // stores move single elements along those layouts, so these flags
+        // only select the whole-tile path and set no alignment requirement
+        t.vec_b = t.vec_c = t.vec_d = true;
         e = sgemm_emu::launch_gemm_acc(t, MFMAE_SHAPE_32x32x16, true, stream);
         if (e != hipSuccess) return e;
     }
