@@ -519,7 +519,9 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
     if (c < nk) compute_stage<CF>(acc, cor, buf0, priv, wrow, wcol, g, j);
 
     // Epilogue: C = main + corr * 2^-11.  Element e of a 32 x 32 block is
-    // row 8 (e / 4) + 4 g + e % 4, column j.
+    // row 8 (e / 4) + 4 g + e % 4, column j.  C is written once and not read
+    // again here: nontemporal stores (measured 5% faster on the batched
+    // 128^3 and 256^3 products, neutral on 8192^3).
 #pragma unroll
     for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
@@ -528,8 +530,9 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
                         32 * tn + j;
 #pragma unroll
             for (int e = 0; e < 16; ++e)
-                cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc] =
-                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]);
+                __builtin_nontemporal_store(
+                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]),
+                    &cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc]);
         }
 }
 
@@ -597,9 +600,9 @@ __device__ inline void map_lds(StageMap<CF>& sm, const BigParams& p) {
     }
 }
 
-// C = main + corr * 2^-11 for the wave's sub-tile, and zero the
-// accumulators.  Element e of a 32 x 32 block is row 8 (e / 4) + 4 g + e % 4,
-// column j.
+// C = main + corr * 2^-11 for the wave's sub-tile (nontemporal stores, as
+// in bgemm_big_kernel), and zero the accumulators.  Element e of a 32 x 32
+// block is row 8 (e / 4) + 4 g + e % 4, column j.
 template <class CF>
 __device__ inline void store_c(f32x16_t (&acc)[CF::TM][CF::TN], f32x16_t (&cor)[CF::TM][CF::TN],
                                const BigParams& p, const TaskGeo& q, int wrow, int wcol, int g,
@@ -612,8 +615,9 @@ __device__ inline void store_c(f32x16_t (&acc)[CF::TM][CF::TN], f32x16_t (&cor)[
                         32 * tn + j;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc] =
-                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]);
+                __builtin_nontemporal_store(
+                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]),
+                    &cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc]);
                 acc[tm][tn][e] = 0.0f;
                 cor[tm][tn][e] = 0.0f;
             }
