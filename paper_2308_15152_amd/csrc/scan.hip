@@ -142,7 +142,10 @@ __device__ inline void scan_block(const Block& b, const half8_t (&Ut)[2], float&
 }
 
 // Outputs in the accumulator layout, regrouped through the wave's LDS
-// buffer and stored as four contiguous 1 KiB instructions.
+// buffer and stored as four contiguous 1 KiB instructions, nontemporal: y
+// is not read again (measured 2.7% faster; the rule-built kernels, whose
+// output stores interleave with the next item's loads, ran 2-3% slower
+// with them).
 __device__ inline void store_fast(float* row, int c0, const float (&y)[16], float* buf) {
     const int l = threadIdx.x & 63;
     float* q = buf + kSegPitch * (l & 31) + 4 * (l >> 5);
@@ -154,8 +157,8 @@ __device__ inline void store_fast(float* row, int c0, const float (&y)[16], floa
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront", "local");
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<f32x4*>(row + c0 + 256 * i + 4 * l) =
-            *reinterpret_cast<const f32x4*>(buf + staged(256 * i + 4 * l));
+        __builtin_nontemporal_store(*reinterpret_cast<const f32x4*>(buf + staged(256 * i + 4 * l)),
+                                    reinterpret_cast<f32x4*>(row + c0 + 256 * i + 4 * l));
 }
 
 __device__ inline void store_bounded(float* row, int c0, int len, const float (&y)[16]) {
