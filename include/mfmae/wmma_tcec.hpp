@@ -32,7 +32,10 @@
 // fragment API requires for 32-bit elements): along the contiguous direction
 // each lane then moves 8 (A, B) or 4 (accumulator) elements with 16-byte
 // accesses.  The *_bounded variants take any p and ld, touch only elements
-// with i < rows and j < cols, and read the others as zero.
+// with i < rows and j < cols, and read the others as zero.  The stores take an
+// optional last argument `nontemporal` (default false): true marks the writes
+// as streaming, for output that is not read again soon; the values written
+// are the same either way.
 #pragma once
 
 #include "frag.hpp"
@@ -86,6 +89,15 @@ struct use_of<accumulator> {
 };
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// one store, streaming (nontemporal) or ordinary
+template <class T>
+__device__ inline void put(T* q, T v, bool nontemporal) {
+    if (nontemporal)
+        __builtin_nontemporal_store(v, q);
+    else
+        *q = v;
+}
 
 }  // namespace detail
 
@@ -290,7 +302,8 @@ __device__ inline void load_matrix_bounded(fragment<accumulator, M, N, K, float,
 template <int M, int N, int K, class P>
 __device__ inline void store_matrix_sync(float* p,
                                          const fragment<accumulator, M, N, K, float, void, P>& f,
-                                         unsigned ld, layout_t layout) {
+                                         unsigned ld, layout_t layout,
+                                         bool nontemporal = false) {
     using Map = typename fragment<accumulator, M, N, K, float, void, P>::map_t;
     const int l = lane_id();
     if (layout == mem_col_major) {
@@ -299,20 +312,22 @@ __device__ inline void store_matrix_sync(float* p,
             detail::f32x4 v;
 #pragma unroll
             for (int t = 0; t < 4; ++t) v[t] = get_element(f, 4 * q + t);
-            *reinterpret_cast<detail::f32x4*>(
-                p + detail::offset<col_major>(Map::row(l, 4 * q), Map::col(l, 4 * q), ld)) = v;
+            detail::put(reinterpret_cast<detail::f32x4*>(p + detail::offset<col_major>(
+                            Map::row(l, 4 * q), Map::col(l, 4 * q), ld)),
+                        v, nontemporal);
         }
     } else {
 #pragma unroll
         for (int e = 0; e < f.num_elements; ++e)
-            p[detail::offset<row_major>(Map::row(l, e), Map::col(l, e), ld)] = get_element(f, e);
+            detail::put(&p[detail::offset<row_major>(Map::row(l, e), Map::col(l, e), ld)],
+                        get_element(f, e), nontemporal);
     }
 }
 
 template <int M, int N, int K, class P>
 __device__ inline void store_matrix_bounded(
     float* p, const fragment<accumulator, M, N, K, float, void, P>& f, int64_t ld,
-    layout_t layout, int rows, int cols) {
+    layout_t layout, int rows, int cols, bool nontemporal = false) {
     using Map = typename fragment<accumulator, M, N, K, float, void, P>::map_t;
     const int l = lane_id();
 #pragma unroll
@@ -320,7 +335,7 @@ __device__ inline void store_matrix_bounded(
         const int i = Map::row(l, e), j = Map::col(l, e);
         const int64_t o = layout == mem_col_major ? detail::offset<col_major>(i, j, ld)
                                                   : detail::offset<row_major>(i, j, ld);
-        if (i < rows && j < cols) p[o] = get_element(f, e);
+        if (i < rows && j < cols) detail::put(&p[o], get_element(f, e), nontemporal);
     }
 }
 
