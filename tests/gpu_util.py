@@ -68,3 +68,42 @@ def gate(C, ref, k, label="", max_gate=True):
 def to_np(t: torch.Tensor) -> np.ndarray:
     torch.cuda.synchronize()
     return t.detach().cpu().numpy()
+
+
+# ---------------------------------------------------------------------------
+# Batches past one launch.  The launchers split a batch into pieces below
+# 2^31 work-items; to cross that boundary with the memory of one device, a
+# pool of P items checked against the oracle is repeated across the batch
+# (item t holds pool item t mod P), and every output item is compared bit for
+# bit with the pool item it repeats: an item the kernel left unwritten (the
+# output starts as NaN), wrote twice or computed from another item's operands
+# breaks the period.
+# ---------------------------------------------------------------------------
+
+def periodic_batch(pool: torch.Tensor, batch: int) -> torch.Tensor:
+    """[batch, ...] on the pool's device: item t is pool[t % P]."""
+    P = pool.shape[0]
+    reps = (batch + P - 1) // P
+    return pool.repeat(reps, *([1] * (pool.dim() - 1)))[:batch]
+
+
+def assert_periodic(C: torch.Tensor, P: int, label: str = "", slab_items: int = 1 << 22):
+    """Every item of C equals item t mod P, bitwise (compared on the device
+    in slabs of whole periods)."""
+    flat = C.reshape(C.shape[0], -1).view(torch.int32)
+    head = flat[:P]
+    per = max(1, slab_items // P) * P
+    for t0 in range(0, flat.shape[0], per):
+        s = flat[t0:t0 + per]
+        q, r = divmod(s.shape[0], P)
+        if q:
+            body = s[:q * P].view(q, P, -1)
+            bad = (body != head.unsqueeze(0)).any(dim=2)
+            if bool(bad.any()):
+                first = int(bad.flatten().nonzero()[0])
+                raise AssertionError(f"{label}: item {t0 + first} differs from pool item "
+                                     f"{first % P}")
+        if r:
+            if not torch.equal(s[q * P:], head[:r]):
+                raise AssertionError(f"{label}: an item in [{t0 + q * P}, {t0 + s.shape[0]}) "
+                                     f"differs from its pool item")

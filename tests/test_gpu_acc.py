@@ -22,7 +22,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import device, gate, to_np
+from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -161,3 +161,25 @@ def test_error_correction_policy(s):
     hiB = B.numpy().astype(np.float16).astype(np.float64)
     hh = np.einsum("bik,bkj->bij", hiA, hiB) + C.numpy().astype(np.float64)
     assert np.all(np.abs(off - hh) <= 130 * 2.0 ** -23 * ref["n64"])
+
+
+def test_batch_past_one_launch():
+    """A batch larger than one launch holds: each wave takes one item of at
+    most 64 x 64, four waves a workgroup, so a launch takes at most
+    (2^31 / 256 - 1) * 4 = 33,554,428 items and this batch needs two.  A pool
+    of P items (k with a tail after one full step) is checked against the
+    oracle and repeated across the batch; every item of D must equal its pool
+    item bitwise."""
+    P, m, n, k = 1021, 2, 3, 20
+    per_launch = ((1 << 31) // 256 - 1) * 4
+    batch = per_launch + 2 * P + 7
+    print(f"case acc batch={batch} m={m} n={n} k={k}", flush=True)
+    dev = device()
+    A, B, C = _draw(P, m, n, k, seed=89)
+    Ad = periodic_batch(A.to(dev), batch)
+    Bd = periodic_batch(B.to(dev), batch)
+    Cd = periodic_batch(C.to(dev), batch)
+    D = torch.full((batch, m, n), float("nan"), device=dev)
+    pkg.sgemm_emu_batched_acc(Ad, Bd, Cd, D)
+    gate(to_np(D[:P]), oracle.gemm_acc(A.numpy(), B.numpy(), C.numpy()), k, "acc pool")
+    assert_periodic(D, P, "acc batch")

@@ -22,7 +22,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import device, gate, gate_applies, to_np
+from gpu_util import assert_periodic, device, gate, gate_applies, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -417,3 +417,27 @@ def test_tiled_ragged_large(shape):
 @pytest.mark.parametrize("shape", REG_SHAPES, ids=lambda s: "x".join(map(str, s)))
 def test_register_flow_ragged_large(shape):
     _check_sampled(shape, "bgemm_reg_kernel", "register flow")
+
+
+def test_register_flow_batch_past_one_launch():
+    """A batch of small products larger than one launch holds: the 64 x 64
+    register-flow tile is one 256-thread workgroup per item, so a launch
+    takes at most 2^31 / 256 - 1 = 8,388,607 items and this batch needs two.
+    A pool of P items (k with a tail after two full steps) is checked against
+    the oracle and repeated across the batch; every item must equal its pool
+    item bitwise."""
+    P, m, n, k = 1021, 2, 3, 36
+    per_launch = (1 << 31) // 256 - 1
+    batch = per_launch + 2 * P + 7
+    print(f"case register flow batch={batch} m={m} n={n} k={k}", flush=True)
+    dev = device()
+    A, B = synth.gemm_inputs(P, m, n, k, seed=97)
+    Ad = periodic_batch(A.to(dev), batch)
+    Bd = periodic_batch(B.to(dev), batch)
+    C = torch.full((batch, m, n), float("nan"), device=dev)
+    pol, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, C)
+    assert kern == "bgemm_reg_kernel" and pol.tile == pkg.TILE_64x64, (pol, kern)
+    pkg.sgemm_emu_batched(Ad, Bd, C)
+    head = to_np(C[:P])
+    gate(head, oracle.gemm(A.numpy(), B.numpy()), k, "register flow pool")
+    assert_periodic(C, P, "register flow batch")

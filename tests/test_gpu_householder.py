@@ -20,7 +20,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import device, gate, to_np
+from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -131,3 +131,25 @@ def test_reflector_split_of_a_binary16_tie(mode):
     C = _run(u, B, mode=mode)
     cm = oracle.householder(u.numpy(), B.numpy(), want=("cm",))["cm"]
     assert np.array_equal(C[0, 0].view(np.uint32), cm[0, 0].astype(np.float32).view(np.uint32))
+
+
+def test_batch_past_one_launch():
+    """A batch larger than one launch holds: each wave takes one item (up to
+    64 columns), four waves a workgroup, so a launch takes at most
+    (2^31 / 256 - 1) * 4 = 33,554,428 items and this batch needs two.  A pool
+    of P items is checked against the oracle and repeated across the batch;
+    every item must equal its pool item bitwise."""
+    P, ncols = 1021, 2
+    per_launch = ((1 << 31) // 256 - 1) * 4
+    batch = per_launch + 2 * P + 7
+    print(f"case householder batch={batch} ncols={ncols}", flush=True)
+    dev = device()
+    u, B = synth.householder_inputs(P, 64, ncols, seed=43)
+    ud = periodic_batch(u.to(dev), batch)
+    Bd = periodic_batch(B.to(dev), batch)
+    C = torch.full((batch, 64, ncols), float("nan"), device=dev)
+    pkg.householder_emu_batched(ud, Bd, C)
+    gate(to_np(C[:P]), oracle.householder(u.numpy(), B.numpy()), 64, "householder pool")
+    assert_periodic(C, P, "householder batch")
+    del ud, Bd, C
+    torch.cuda.empty_cache()
