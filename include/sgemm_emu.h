@@ -44,7 +44,10 @@ extern "C" {
 #define SGEMM_EMU_ERR_DIM (-1)         /* negative m, n, k, batch or ncols    */
 #define SGEMM_EMU_ERR_LD (-2)          /* leading dimension too small          */
 #define SGEMM_EMU_ERR_NULL (-3)        /* NULL pointer with nonzero work       */
-#define SGEMM_EMU_ERR_STRIDE (-4)      /* negative stride, or C items overlap  */
+#define SGEMM_EMU_ERR_STRIDE (-4)      /* negative stride, C items overlap, or
+                                          an operand's span (strides and ld)
+                                          runs past the end of the address
+                                          space                               */
 #define SGEMM_EMU_ERR_ALIAS (-5)       /* C overlaps A or B (or u)             */
 #define SGEMM_EMU_ERR_UNSUPPORTED (-6) /* size outside what an entry supports  */
 #define SGEMM_EMU_ERR_HIP (-7)         /* the HIP runtime reported an error    */
@@ -306,7 +309,7 @@ int givens_emu_batched(int n, int i, int j,
  * Batched inclusive scan through a rule-built matrix (Sec. 4.1, eq.
  * scan-mat): for every row r in [0, rows),
  *   Y[r][j] := sum_{i <= j} X[r][i],   j in [0, len)
- computed with the upper-triangular all-ones matrix U (u_ij = 1 for
+ * computed with the upper-triangular all-ones matrix U (u_ij = 1 for
  * i <= j), whose operand fragments are generated from that rule with
  * foreach_ij, in emulated FP32 (Sec. 4.4): each block of 1024 values is
  * taken as 32 segments of 32, scanned within segments by one product with
@@ -315,9 +318,10 @@ int givens_emu_batched(int n, int i, int j,
  * ldy.  Y may be X itself (ldy == ldx) for an in-place scan; any other
  * overlap is an error.  Rows are independent; a wavefront scans 8 rows, so
  * parallelism comes from the number of rows.  Rows of a multiple of 1024
- * values with 16-byte aligned X and Y rows take 16-byte accesses.
- * Supported: rows < 2^30 (else SGEMM_EMU_ERR_UNSUPPORTED).
- * Errors: SGEMM_EMU_ERR_DIM, _LD, _NULL, _ALIAS, _UNSUPPORTED, _HIP.
+ * values with 16-byte aligned X and Y rows take 16-byte accesses.  Any
+ * number of rows: more than 268,435,424 take several launches.
+ * Errors: SGEMM_EMU_ERR_DIM, _LD (also when rows x ld runs past the end of
+ * the address space), _NULL, _ALIAS, _HIP.
  */
 int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx,
                    float* Y, int64_t ldy, hipStream_t stream);
@@ -327,7 +331,8 @@ int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx,
  * device: hi[i], lo[i] receive the binary16 bit patterns of
  * toFP16(x[i]) and toFP16((x[i] - toFP32(hi)) * 2^11).  count >= 0; x, hi
  * and lo are device pointers of count elements and must not overlap.
- * Errors: SGEMM_EMU_ERR_DIM, _NULL, _ALIAS, _HIP.
+ * Errors: SGEMM_EMU_ERR_DIM (also when count elements run past the end of
+ * the address space), _NULL, _ALIAS, _HIP.
  */
 int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
                     hipStream_t stream);

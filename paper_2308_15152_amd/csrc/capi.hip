@@ -3,6 +3,8 @@
 // before any HIP call, so every error path is free of side effects.
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "internal.h"
 #include "mfmae/frag.hpp"
 #include "sgemm_emu.h"
@@ -18,16 +20,31 @@ int hip_fail(hipError_t e) {
 
 struct Extent {
     uintptr_t lo, hi;  // [lo, hi) in bytes; empty if lo == hi
+    bool ok;           // false: the span runs past the end of the address space
 };
 
 // Bytes spanned by `items` row-major matrices of rows x cols with leading
-// dimension ld and item stride s (elements), starting at p.
-Extent extent(const void* p, int64_t items, int64_t rows, int64_t cols, int64_t ld, int64_t s) {
-    Extent e{(uintptr_t)p, (uintptr_t)p};
+// dimension ld and item stride s (elements of `elem` bytes), starting at p.
+// All arguments are non-negative; the span is computed in 128 bits, so no
+// stride or leading dimension can wrap it.
+Extent extent(const void* p, int64_t items, int64_t rows, int64_t cols, int64_t ld, int64_t s,
+              int64_t elem = sizeof(float)) {
+    Extent e{(uintptr_t)p, (uintptr_t)p, true};
     if (items <= 0 || rows <= 0 || cols <= 0) return e;
-    const int64_t last = (items - 1) * s + (rows - 1) * ld + cols;  // elements
-    e.hi = e.lo + (uintptr_t)last * sizeof(float);
+    const __int128 last = (__int128)(items - 1) * s + (__int128)(rows - 1) * ld + cols;
+    const __int128 bytes = last * elem;
+    if (bytes > (__int128)(UINTPTR_MAX - e.lo)) {
+        e.ok = false;
+        return e;
+    }
+    e.hi = e.lo + (uintptr_t)bytes;
     return e;
+}
+
+bool all_ok(std::initializer_list<Extent> es) {
+    for (const Extent& e : es)
+        if (!e.ok) return false;
+    return true;
 }
 
 bool overlap(Extent a, Extent b) {
@@ -56,9 +73,11 @@ int check_gemm(int m, int n, int k, const float* A, int lda, const float* B, int
     if (st.a < 0 || st.b < 0 || st.c < 0) return SGEMM_EMU_ERR_STRIDE;
     if (batch > 1 && st.c < (int64_t)(m - 1) * ldc + n) return SGEMM_EMU_ERR_STRIDE;
     const Extent ec = extent(C, batch, m, n, ldc, st.c);
+    if (!ec.ok) return SGEMM_EMU_ERR_STRIDE;
     if (k > 0) {
         const Extent ea = extent(A, st.a == 0 ? 1 : batch, m, k, lda, st.a);
         const Extent eb = extent(B, st.b == 0 ? 1 : batch, k, n, ldb, st.b);
+        if (!all_ok({ea, eb})) return SGEMM_EMU_ERR_STRIDE;
         if (overlap(ec, ea) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
     }
     return SGEMM_EMU_OK;
@@ -404,12 +423,14 @@ int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k
     if (stride.a < 0 || stride.b < 0 || stride.c < 0 || stride.d < 0) return SGEMM_EMU_ERR_STRIDE;
     if (batch > 1 && stride.d < (int64_t)(cr - 1) * ldd + cc) return SGEMM_EMU_ERR_STRIDE;
     const Extent ed = extent(D, batch, cr, cc, ldd, stride.d);
-    const Extent ea = k > 0 ? extent(A, stride.a == 0 ? 1 : batch, ar, ac, lda, stride.a) : Extent{};
-    const Extent eb = k > 0 ? extent(B, stride.b == 0 ? 1 : batch, br, bc, ldb, stride.b) : Extent{};
+    const Extent none{0, 0, true};
+    const Extent ea = k > 0 ? extent(A, stride.a == 0 ? 1 : batch, ar, ac, lda, stride.a) : none;
+    const Extent eb = k > 0 ? extent(B, stride.b == 0 ? 1 : batch, br, bc, ldb, stride.b) : none;
+    const Extent ecx = C ? extent(C, stride.c == 0 ? 1 : batch, cr, cc, ldc, stride.c) : none;
+    if (!all_ok({ed, ea, eb, ecx})) return SGEMM_EMU_ERR_STRIDE;
     if (overlap(ed, ea) || overlap(ed, eb)) return SGEMM_EMU_ERR_ALIAS;
     if (C) {
         const bool in_place = C == D && ldc == ldd && stride.c == stride.d;
-        const Extent ecx = extent(C, stride.c == 0 ? 1 : batch, cr, cc, ldc, stride.c);
         if (!in_place && overlap(ed, ecx)) return SGEMM_EMU_ERR_ALIAS;
     }
     auto vec_ok = [](const void* p, int64_t ld, int64_t s) {
@@ -469,6 +490,7 @@ int householder_emu_batched_ex(int n, const float* u, int64_t stride_u, const fl
     const Extent ec = extent(C, batch, n, ncols, ldc, stride_c);
     const Extent eu = extent(u, stride_u == 0 ? 1 : batch, 1, n, n, stride_u);
     const Extent eb = extent(B, stride_b == 0 ? 1 : batch, n, ncols, ldb, stride_b);
+    if (!all_ok({ec, eu, eb})) return SGEMM_EMU_ERR_STRIDE;
     if (overlap(ec, eu) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
     sgemm_emu::HouseholderArgs a;
     a.mode = mode;
@@ -508,6 +530,7 @@ int givens_emu_batched(int n, int i, int j, const float* c, const float* s, int6
     const Extent ecs = extent(c, stride_cs == 0 ? 1 : batch, 1, 1, 1, stride_cs);
     const Extent ess = extent(s, stride_cs == 0 ? 1 : batch, 1, 1, 1, stride_cs);
     const Extent eb = extent(B, stride_b == 0 ? 1 : batch, n, ncols, ldb, stride_b);
+    if (!all_ok({ec, ecs, ess, eb})) return SGEMM_EMU_ERR_STRIDE;
     if (overlap(ec, ecs) || overlap(ec, ess) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
     sgemm_emu::GivensArgs a;
     a.ncols = ncols;
@@ -533,11 +556,10 @@ int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx, float* Y,
     if (rows < 0 || len < 0) return SGEMM_EMU_ERR_DIM;
     if (ldx < (len > 1 ? len : 1) || ldy < (len > 1 ? len : 1)) return SGEMM_EMU_ERR_LD;
     if (rows == 0 || len == 0) return SGEMM_EMU_OK;
-    // one wave per 32 rows, 4 waves per workgroup, below 2^31 work-items
-    if ((rows + 127) / 128 >= (int64_t(1) << 31) / 256) return SGEMM_EMU_ERR_UNSUPPORTED;
     if (X == nullptr || Y == nullptr) return SGEMM_EMU_ERR_NULL;
     const Extent ex = extent(X, 1, rows, len, ldx, 0);
     const Extent ey = extent(Y, 1, rows, len, ldy, 0);
+    if (!all_ok({ex, ey})) return SGEMM_EMU_ERR_LD;
     const bool in_place = X == Y && ldx == ldy;
     if (!in_place && overlap(ex, ey)) return SGEMM_EMU_ERR_ALIAS;
     sgemm_emu::ScanArgs a;
@@ -558,9 +580,10 @@ int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
     if (count < 0) return SGEMM_EMU_ERR_DIM;
     if (count == 0) return SGEMM_EMU_OK;
     if (x == nullptr || hi == nullptr || lo == nullptr) return SGEMM_EMU_ERR_NULL;
-    const Extent ex{(uintptr_t)x, (uintptr_t)x + (uintptr_t)count * 4};
-    const Extent eh{(uintptr_t)hi, (uintptr_t)hi + (uintptr_t)count * 2};
-    const Extent el{(uintptr_t)lo, (uintptr_t)lo + (uintptr_t)count * 2};
+    const Extent ex = extent(x, 1, 1, count, count, 0, 4);
+    const Extent eh = extent(hi, 1, 1, count, count, 0, 2);
+    const Extent el = extent(lo, 1, 1, count, count, 0, 2);
+    if (!all_ok({ex, eh, el})) return SGEMM_EMU_ERR_DIM;
     if (overlap(ex, eh) || overlap(ex, el) || overlap(eh, el)) return SGEMM_EMU_ERR_ALIAS;
     hipError_t e = sgemm_emu::launch_split(count, x, hi, lo, stream);
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);

@@ -261,11 +261,23 @@ __global__ __launch_bounds__(64 * kWaves, 2) void scan_kernel(ScanArgs p) {
 }  // namespace
 
 hipError_t launch_scan(const ScanArgs& a, hipStream_t stream) {
-    const int64_t waves = (a.rows + kRowsPerWave - 1) / kRowsPerWave;
-    const int64_t blocks = (waves + kWaves - 1) / kWaves;
-    if (blocks >= (int64_t(1) << 31) / (64 * kWaves)) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(scan_kernel, dim3((unsigned)blocks), dim3(64 * kWaves), 0, stream, a);
-    return hipGetLastError();
+    // one launch stays below 2^31 work-items (the dispatch packet counts
+    // work-items in 32 bits); more rows take several launches, each on its
+    // own range of rows
+    const int64_t max_blocks = (int64_t(1) << 31) / (64 * kWaves) - 1;
+    const int64_t rows_per_launch = max_blocks * kWaves * kRowsPerWave;
+    for (int64_t r0 = 0; r0 < a.rows; r0 += rows_per_launch) {
+        ScanArgs c = a;
+        c.rows = a.rows - r0 < rows_per_launch ? a.rows - r0 : rows_per_launch;
+        c.X = a.X + r0 * a.ldx;
+        c.Y = a.Y + r0 * a.ldy;
+        const int64_t waves = (c.rows + kRowsPerWave - 1) / kRowsPerWave;
+        const int64_t blocks = (waves + kWaves - 1) / kWaves;
+        hipLaunchKernelGGL(scan_kernel, dim3((unsigned)blocks), dim3(64 * kWaves), 0, stream, c);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace sgemm_emu

@@ -92,6 +92,10 @@ def test_null_pointers():
 def test_strides():
     assert gemm(4, 4, 4, batch=2, st=(-16, 16, 16)) == -4
     assert gemm(4, 4, 4, batch=2, st=(16, 16, 15)) == -4  # C items would overlap
+    # spans that run past the end of the address space (computed without wrapping)
+    assert gemm(4, 4, 4, batch=2, st=(16, 16, 1 << 62)) == -4
+    assert gemm(4, 4, 4, batch=2, st=(1 << 62, 16, 16)) == -4
+    assert gemm(4, 4, 4, batch=1 << 30, st=(16, 1 << 34, 16)) == -4
 
 
 def test_aliasing():
@@ -257,6 +261,8 @@ def test_householder_validation():
     assert hh(u=0) == -3
     assert hh(sb=-1) == -4
     assert hh(sc=100) == -4
+    assert hh(su=1 << 62) == -4
+    assert hh(sc=1 << 62) == -4
     assert hh(C=PB) == -5
     assert hh(C=PA + 4) == -5
     assert hh(batch=0) == 0
@@ -302,6 +308,8 @@ def test_givens_validation():
     assert gv(scs=-1) == -4
     assert gv(sb=-1) == -4
     assert gv(sc=100) == -4
+    assert gv(scs=1 << 62) == -4
+    assert gv(sb=1 << 62) == -4
     assert gv(C=PB) == -5
     assert gv(C=PA - 4) == -5
     assert gv(C=PS - 64 * 64 * 4 + 8) == -5
@@ -352,6 +360,9 @@ def test_batched_acc_validation():
     assert acc(A=0, B=0, k=0) == -4           # k = 0 reads neither
     ok = (64 * 32, 32 * 48, 64 * 48, 64 * 48)
     assert acc(st=(0, 0, 0, 100)) == -4       # D items overlap
+    assert acc(st=(1 << 62, 0, 0, 64 * 48)) == -4  # A's span past the address space
+    assert acc(st=(0, 0, 1 << 62, 64 * 48)) == -4
+    assert acc(st=(0, 0, 0, 1 << 62)) == -4
     assert acc(st=ok, D=PB + 4) == -5
     assert acc(st=ok, D=PA) == -5
     assert acc(st=ok, D=PC + 8) == -5         # partial overlap with C
@@ -371,7 +382,9 @@ def test_scan_validation():
     assert sc(ldy=0) == -2
     assert sc(rows=0) == 0
     assert sc(length=0) == 0
-    assert sc(rows=1 << 30) == -6
+    # rows x ld past the end of the address space (computed without wrapping)
+    assert sc(rows=1 << 40, ldx=1 << 30) == -2
+    assert sc(rows=2, ldy=1 << 62) == -2
     assert sc(X=0) == -3
     assert sc(Y=0) == -3
     assert sc(Y=PA + 4) == -5
@@ -385,6 +398,7 @@ def test_split_validation():
     assert lib.sgemm_emu_split(0, P(0), P(0), P(0), P(0)) == 0
     assert lib.sgemm_emu_split(16, P(0), P(PB), P(PC), P(0)) == -3
     assert lib.sgemm_emu_split(16, P(PA), P(PA + 8), P(PC), P(0)) == -5
+    assert lib.sgemm_emu_split(1 << 62, P(PA), P(PB), P(PC), P(0)) == -1
 
 
 def test_strerror_covers_codes():

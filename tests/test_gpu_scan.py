@@ -28,7 +28,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import device, gate, to_np
+from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -108,3 +108,23 @@ def test_workload_scan_sampled():
     ref = oracle.scan(X[rows].numpy())
     e = gate(Ys, ref, _k_eff(w.n), "scan_2048", max_gate=False)
     print(f"scan_2048: err {e[0]:.3e} fp32 running sum {e[1]:.3e}")
+
+
+def test_rows_past_one_launch():
+    """More rows than one launch holds: a wave scans 8 rows, four waves a
+    workgroup, so a launch takes at most (2^31 / 256 - 1) * 32 = 268,435,424
+    rows and this scan needs two.  A pool of P rows is checked against the
+    oracle and repeated down the rows; every output row must equal its pool
+    row bitwise."""
+    P, length = 1021, 5
+    per_launch = ((1 << 31) // 256 - 1) * 32
+    rows = per_launch + 2 * P + 7
+    print(f"case scan rows={rows} len={length}", flush=True)
+    X = synth.uniform((P, length), synth.rng(99))
+    Xd = periodic_batch(X.to(device()), rows)
+    Y = torch.full((rows, length), float("nan"), device=device())
+    pkg.sgemm_emu_scan(Xd, Y)
+    gate(to_np(Y[:P]), oracle.scan(X.numpy()), _k_eff(length), "scan pool", max_gate=False)
+    assert_periodic(Y, P, "scan rows")
+    del Xd, Y
+    torch.cuda.empty_cache()
