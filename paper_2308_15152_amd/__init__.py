@@ -13,6 +13,7 @@ correction products in their own accumulator, and C = main + corr * 2^-11.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -81,6 +82,7 @@ class Policy(ctypes.Structure):
 
 
 _lib = None
+_NO_SWITCH = contextlib.nullcontext()
 
 
 def lib_path() -> str:
@@ -162,6 +164,35 @@ def _ptr(t) -> ctypes.c_void_p:
     return ctypes.c_void_p(0 if t is None else int(t.data_ptr()))
 
 
+def _on_device(*ts):
+    """Context for a launch on the tensors' device: every tensor given (None
+    skipped) must be a device tensor of one device, which is made current so
+    that the kernels and the current stream are that device's."""
+    import torch
+
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("every operand must be a device tensor")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"operands on different devices: {dev} and {t.device}")
+    if dev is None or dev.index == torch.cuda.current_device():
+        return _NO_SWITCH
+    return torch.cuda.device(dev)
+
+
+def _check_shape(t, shape, name: str) -> None:
+    """An output the caller passes must have exactly the shape the call
+    writes: the library writes every element of that shape and cannot see
+    the allocation behind the pointer."""
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
 def _matrix_view(t, name: str):
     """(batch, rows, cols, ld, batch_stride) of a 2-D or 3-D FP32 tensor whose
     rows are contiguous."""
@@ -217,14 +248,15 @@ def sgemm_emu_batched(A, B, C=None, *, policy: Policy | None = None, stream=None
     to sgemm_emu_batched_ex."""
     m, n, k, lda, ldb, ldc, batch, st, C = _gemm_args(A, B, C)
     lib = load()
-    if policy is None:
-        rc = lib.sgemm_emu_batched(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
-                                   st, _stream(stream))
-        _check(rc, "sgemm_emu_batched")
-    else:
-        rc = lib.sgemm_emu_batched_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
-                                      st, ctypes.byref(policy), _stream(stream))
-        _check(rc, "sgemm_emu_batched_ex")
+    with _on_device(A, B, C):
+        if policy is None:
+            rc = lib.sgemm_emu_batched(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, batch,
+                                       st, _stream(stream))
+            _check(rc, "sgemm_emu_batched")
+        else:
+            rc = lib.sgemm_emu_batched_ex(m, n, k, _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc,
+                                          batch, st, ctypes.byref(policy), _stream(stream))
+            _check(rc, "sgemm_emu_batched_ex")
     return C
 
 
@@ -281,9 +313,10 @@ def sgemm_emu_batched_acc(A, B, C=None, D=None, *, op_a: int = OP_N, op_b: int =
         if (cr, ccol) != stored or (bcx is not None and bcx != batch):
             raise ValueError("C has the wrong shape")
     st = Stride4(sa, sb, sc, sd)
-    rc = load().sgemm_emu_batched_acc(int(op_a), int(op_b), int(layout), m, n, k, _ptr(A), lda,
-                                      _ptr(B), ldb, _ptr(C), ldc, _ptr(D), ldd, batch, st,
-                                      int(shape), int(ec), _stream(stream))
+    with _on_device(A, B, C, D):
+        rc = load().sgemm_emu_batched_acc(int(op_a), int(op_b), int(layout), m, n, k, _ptr(A),
+                                          lda, _ptr(B), ldb, _ptr(C), ldc, _ptr(D), ldd, batch,
+                                          st, int(shape), int(ec), _stream(stream))
     _check(rc, "sgemm_emu_batched_acc")
     return D
 
@@ -321,7 +354,8 @@ def sgemm_emu_scan(X, Y=None, *, stream=None):
         if not Y.is_contiguous():
             raise ValueError("Y must be contiguous (or 2-D with contiguous rows)")
         ldy = max(length, 1)
-    rc = load().sgemm_emu_scan(rows, length, _ptr(X), ldx, _ptr(Y), ldy, _stream(stream))
+    with _on_device(X, Y):
+        rc = load().sgemm_emu_scan(rows, length, _ptr(X), ldx, _ptr(Y), ldy, _stream(stream))
     _check(rc, "sgemm_emu_scan")
     return Y
 
@@ -342,10 +376,14 @@ def householder_emu_batched(u, B, C=None, *, mode: int = HOUSEHOLDER_RULE, strea
         raise ValueError("B must be [batch, n, ncols]")
     if C is None:
         C = torch.empty((batch, n, ncols), dtype=torch.float32, device=u.device)
+    _check_shape(C, (batch, n, ncols) if C.dim() == 3 else (n, ncols), "C")
+    if C.dim() == 2 and batch != 1:
+        raise ValueError("a 2-D C holds one item")
     _, _, _, ldc, sc = _matrix_view(C, "C")
     su = u.stride(0) if batch > 1 else 0
-    rc = load().householder_emu_batched_ex(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C),
-                                           ldc, sc, batch, int(mode), _stream(stream))
+    with _on_device(u, B, C):
+        rc = load().householder_emu_batched_ex(n, _ptr(u), su, _ptr(B), ldb, sb, ncols, _ptr(C),
+                                               ldc, sc, batch, int(mode), _stream(stream))
     _check(rc, "householder_emu_batched_ex")
     return C
 
@@ -370,10 +408,15 @@ def givens_emu_batched(i, j, c, s, B, C=None, *, mode: int = GIVENS_AUTO, stream
         raise ValueError("B must be [batch, n, ncols]")
     if C is None:
         C = torch.empty((batch, n, ncols), dtype=torch.float32, device=B.device)
+    _check_shape(C, (batch, n, ncols) if C.dim() == 3 else (n, ncols), "C")
+    if C.dim() == 2 and batch != 1:
+        raise ValueError("a 2-D C holds one item")
     _, _, _, ldc, sc = _matrix_view(C, "C")
     scs = c.stride(0) if batch > 1 else 0
-    rc = load().givens_emu_batched(n, int(i), int(j), _ptr(c), _ptr(s), scs, _ptr(B), ldb, sb,
-                                   ncols, _ptr(C), ldc, sc, batch, int(mode), _stream(stream))
+    with _on_device(c, s, B, C):
+        rc = load().givens_emu_batched(n, int(i), int(j), _ptr(c), _ptr(s), scs, _ptr(B), ldb,
+                                       sb, ncols, _ptr(C), ldc, sc, batch, int(mode),
+                                       _stream(stream))
     _check(rc, "givens_emu_batched")
     return C
 
@@ -387,7 +430,8 @@ def sgemm_emu_split(x, *, stream=None):
         raise ValueError("x must be a contiguous float32 device tensor")
     hi = torch.empty(x.shape, dtype=torch.int16, device=x.device)
     lo = torch.empty(x.shape, dtype=torch.int16, device=x.device)
-    rc = load().sgemm_emu_split(x.numel(), _ptr(x), _ptr(hi), _ptr(lo), _stream(stream))
+    with _on_device(x, hi, lo):
+        rc = load().sgemm_emu_split(x.numel(), _ptr(x), _ptr(hi), _ptr(lo), _stream(stream))
     _check(rc, "sgemm_emu_split")
     return hi, lo
 
@@ -421,7 +465,13 @@ def mfmae_mma_probe(shape: int, a_lanes, b_lanes, *, stream=None):
     import torch
 
     n = mfmae_num_elements(shape, USE_ACC)
+    for name, t in (("a_lanes", a_lanes), ("b_lanes", b_lanes)):
+        if t.dtype != torch.int16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous int16 device tensor")
+        _check_shape(t, (64, 8), name)
     d = torch.empty((64, n), dtype=torch.float32, device=a_lanes.device)
-    rc = load().mfmae_mma_probe(shape, _ptr(a_lanes), _ptr(b_lanes), _ptr(d), _stream(stream))
+    with _on_device(a_lanes, b_lanes, d):
+        rc = load().mfmae_mma_probe(shape, _ptr(a_lanes), _ptr(b_lanes), _ptr(d),
+                                    _stream(stream))
     _check(rc, "mfmae_mma_probe")
     return d

@@ -1,0 +1,60 @@
+"""The Python binding's own checks, on device tensors: an output the caller
+passes must have the shape the call writes (the library cannot see the
+allocation behind a pointer), probe operands must be [64, 8] int16, and
+every operand must be a device tensor.  Each rejected call raises before
+anything is launched, and the output is left untouched."""
+import pytest
+import torch
+
+import paper_2308_15152_amd as pkg
+from gpu_util import device
+
+pytestmark = pytest.mark.gpu
+
+
+def test_householder_rejects_wrong_output_shape():
+    dev = device()
+    u = torch.nn.functional.normalize(torch.randn(3, 64, device=dev), dim=1)
+    B = torch.rand(3, 64, 10, device=dev)
+    for shape in [(3, 64, 9), (2, 64, 10), (3, 63, 10), (64, 10)]:
+        C = torch.full(shape, 5.0, device=dev)
+        with pytest.raises(ValueError):
+            pkg.householder_emu_batched(u, B, C)
+        assert bool((C == 5.0).all())
+    C = torch.empty(3, 64, 10, device=dev)
+    pkg.householder_emu_batched(u, B, C)  # the right shape still runs
+    torch.cuda.synchronize()
+
+
+def test_givens_rejects_wrong_output_shape():
+    dev = device()
+    c = torch.full((4,), 0.6, device=dev)
+    s = torch.full((4,), 0.8, device=dev)
+    B = torch.rand(4, 64, 8, device=dev)
+    for shape in [(4, 64, 7), (3, 64, 8), (64, 8)]:
+        C = torch.full(shape, 5.0, device=dev)
+        with pytest.raises(ValueError):
+            pkg.givens_emu_batched(5, 37, c, s, B, C)
+        assert bool((C == 5.0).all())
+
+
+def test_probe_rejects_bad_operands():
+    dev = device()
+    ok = torch.zeros(64, 8, dtype=torch.int16, device=dev)
+    for bad in [torch.zeros(64, 4, dtype=torch.int16, device=dev),
+                torch.zeros(32, 8, dtype=torch.int16, device=dev),
+                torch.zeros(64, 8, dtype=torch.float16, device=dev),
+                torch.zeros(8, 64, dtype=torch.int16, device=dev).t()]:
+        with pytest.raises(ValueError):
+            pkg.mfmae_mma_probe(pkg.SHAPE_32x32x16, bad, ok)
+        with pytest.raises(ValueError):
+            pkg.mfmae_mma_probe(pkg.SHAPE_32x32x16, ok, bad)
+
+
+def test_operands_must_be_device_tensors():
+    dev = device()
+    A = torch.rand(2, 8, 8, device=dev)
+    with pytest.raises((ValueError, TypeError)):
+        pkg.sgemm_emu_batched(A, torch.rand(2, 8, 8))
+    with pytest.raises(ValueError):
+        pkg.sgemm_emu_scan(torch.rand(4, 8))
