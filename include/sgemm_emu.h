@@ -128,7 +128,8 @@ int sgemm_emu_batched(int m, int n, int k,
  *                         and n multiples of 4) or else of 2 (8-byte
  *                         aligned, even); tiles 64x64 and 128x128 only.
  *                         Otherwise SGEMM_EMU_ERR_POLICY.
- * ec:   1 = error correction (3 products), 0 = hi.hi only (accuracy control).
+ * ec:   1 = error correction (3 products), 0 = hi.hi only (the comparison
+ *       without correction: accuracy and cost).
  * tile: 0 = automatic, or one of SGEMM_EMU_TILE_*.
  */
 #define SGEMM_EMU_FLOW_AUTO 0
@@ -174,7 +175,11 @@ int sgemm_emu_batched_ex(int m, int n, int k,
  * byte offsets fit in 32 bits ((rows of the tile x lda + 32) x 4 < 2^32 and
  * (32 ldb + columns of the tile) x 4 < 2^32: lda below about 2^30 / tile
  * rows, ldb below about 2^25); otherwise the general LDS kernel (128x256
- * has none: SGEMM_EMU_ERR_POLICY). */
+ * has none: SGEMM_EMU_ERR_POLICY).  Without error correction (ec = 0, for
+ * measuring what the correction costs), the split flow with tile 128x128
+ * or 128x256 runs the same full-tile kernel under the same conditions, and
+ * AUTO picks among those two tiles; the decomposition of large ragged
+ * products is made only with error correction. */
 int sgemm_emu_resolve_policy(int m, int n, int k,
                              const float* A, int lda,
                              const float* B, int ldb,

@@ -76,11 +76,16 @@ enum { BIG_SPLIT = SGEMM_EMU_FLOW_SPLIT, BIG_DIRECT = SGEMM_EMU_FLOW_DIRECT,
        BIG_STAGED = SGEMM_EMU_FLOW_STAGED };
 
 template <int BM_, int BN_, int WAVES_M_, int WAVES_N_, int W_, int VALU_PER_MFMA_ = 0,
-          int FLOW_ = BIG_SPLIT>
+          int FLOW_ = BIG_SPLIT, bool EC_ = true>
 struct BigCfg {
     static constexpr int BM = BM_, BN = BN_, BK = 32;
     static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, W = W_;
     static constexpr int FLOW = FLOW_;
+    // error correction: false keeps the hi.hi product only (staging converts
+    // hi alone; the lo planes are neither written nor read)
+    static constexpr bool EC = EC_;
+    static_assert(EC || FLOW == BIG_SPLIT, "EC off is built for the split flow");
+    static constexpr int MFMAS_PER_BLOCK = EC ? 3 : 1;
     // 0: compiler's own schedule; else the MFMAs of a chunk are interleaved
     // with this many VALU instructions each (the split of the next chunk)
     static constexpr int VALU_PER_MFMA = VALU_PER_MFMA_;
@@ -246,6 +251,20 @@ __device__ inline void store_stage(const Stage<CF>& st, const StageMap<CF>& sm,
     unsigned char* a_lo = buf + CF::A_PLANE;
     unsigned char* b_hi = buf + 2 * CF::A_PLANE;
     unsigned char* b_lo = b_hi + CF::B_PLANE;
+    if constexpr (!CF::EC) {
+#pragma unroll
+        for (int u = 0; u < CF::A_UNITS; ++u) {
+            const half4_t h0 = __builtin_convertvector(st.a[u][0], half4_t);
+            const half4_t h1 = __builtin_convertvector(st.a[u][1], half4_t);
+            *reinterpret_cast<half8_t*>(a_hi + sm.a_lds[u]) =
+                half8_t{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
+        }
+#pragma unroll
+        for (int r = 0; r < CF::B_QUADS; ++r)
+            *reinterpret_cast<half4_t*>(b_hi + sm.bq_lds + r * CF::B_PASS_ROWS * 2 * CF::BN) =
+                __builtin_convertvector(st.bq[r], half4_t);
+        return;
+    }
 #pragma unroll
     for (int u = 0; u < CF::A_UNITS; ++u) {
         const float x[8] = {st.a[u][0][0], st.a[u][0][1], st.a[u][0][2], st.a[u][0][3],
@@ -351,7 +370,7 @@ __device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
             for (int tm = 0; tm < CF::TM; ++tm) {
                 const int o = piece(arow + 32 * tm + j, q);
                 ahi[tm] = *reinterpret_cast<const half8_t*>(a_hi + o);
-                alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
+                if constexpr (CF::EC) alo[tm] = *reinterpret_cast<const half8_t*>(a_lo + o);
             }
             if constexpr (CF::FLOW == BIG_SPLIT) {
                 // lane 16 G + sl reads row 8 (G / 2) + sl / 4 (+ 4 for the
@@ -367,9 +386,12 @@ __device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
                     const int o = bquad<CF>(kl, 8 * ((brow >> 5) + tn) + ql);
                     const int o4 = o + 4 * 2 * CF::BN;  // rows + 4: same swizzle
                     const half4_t h0 = read_tr(b_hi + o), h1 = read_tr(b_hi + o4);
-                    const half4_t l0 = read_tr(b_lo + o), l1 = read_tr(b_lo + o4);
                     bhi[tn] = half8_t{h0[0], h0[1], h0[2], h0[3], h1[0], h1[1], h1[2], h1[3]};
-                    blo[tn] = half8_t{l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+                    if constexpr (CF::EC) {
+                        const half4_t l0 = read_tr(b_lo + o), l1 = read_tr(b_lo + o4);
+                        blo[tn] =
+                            half8_t{l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3]};
+                    }
                 }
             } else {
 #pragma unroll
@@ -386,6 +408,7 @@ __device__ inline void compute_stage(f32x16_t (&acc)[CF::TM][CF::TN],
             for (int tn = 0; tn < CF::TN; ++tn)
                 acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[tm], bhi[tn], acc[tm][tn],
                                                                      0, 0, 0);
+        if constexpr (!CF::EC) continue;
 #pragma unroll
         for (int tm = 0; tm < CF::TM; ++tm)
 #pragma unroll
@@ -407,7 +430,7 @@ template <class CF>
 __device__ inline void interleave() {
     if constexpr (CF::VALU_PER_MFMA > 0) {
 #pragma unroll
-        for (int i = 0; i < 3 * (CF::BK / 16) * CF::TM * CF::TN; ++i) {
+        for (int i = 0; i < CF::MFMAS_PER_BLOCK * (CF::BK / 16) * CF::TM * CF::TN; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
             __builtin_amdgcn_sched_group_barrier(0x002, CF::VALU_PER_MFMA, 0);  // VALU
         }
@@ -531,7 +554,9 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
 #pragma unroll
             for (int e = 0; e < 16; ++e)
                 __builtin_nontemporal_store(
-                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]),
+                    CF::EC ? __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv,
+                                            acc[tm][tn][e])
+                           : acc[tm][tn][e],
                     &cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc]);
         }
 }
@@ -813,6 +838,10 @@ using Big128x128 = BigCfg<128, 128, 2, 2, 2>;
 // the paper's two data flows, for measurement, on the 128 x 128 tile
 using Big128x128Direct = BigCfg<128, 128, 2, 2, 2, 0, BIG_DIRECT>;
 using Big128x128Staged = BigCfg<128, 128, 2, 2, 2, 0, BIG_STAGED>;
+// error correction off (the hi.hi product alone), for measuring what the
+// correction costs on the same kernel and tiles
+using Big128x256NoEC = BigCfg<128, 256, 2, 4, 2, 4, BIG_SPLIT, false>;
+using Big128x128NoEC = BigCfg<128, 128, 2, 2, 2, 0, BIG_SPLIT, false>;
 
 template <class CF>
 bool fits(const GemmArgs& a) {
@@ -822,7 +851,12 @@ bool fits(const GemmArgs& a) {
 
 }  // namespace
 
-bool big_supported(const GemmArgs& a, int tile, int flow) {
+bool big_supported(const GemmArgs& a, int tile, int flow, bool ec) {
+    if (!ec) {
+        if (flow != SGEMM_EMU_FLOW_SPLIT) return false;
+        if (tile == SGEMM_EMU_TILE_128x128) return fits<Big128x128NoEC>(a);
+        return tile == SGEMM_EMU_TILE_128x256 && fits<Big128x256NoEC>(a);
+    }
     if (flow != SGEMM_EMU_FLOW_SPLIT)
         return tile == SGEMM_EMU_TILE_128x128 &&
                (flow == SGEMM_EMU_FLOW_DIRECT || flow == SGEMM_EMU_FLOW_STAGED) &&
@@ -842,8 +876,11 @@ bool big_streams(const GemmArgs& a, int tile, int flow) {
     return flow == SGEMM_EMU_FLOW_SPLIT && tile == SGEMM_EMU_TILE_256x128 && a.k <= 2048;
 }
 
-hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream) {
-    if (!big_supported(a, tile, flow)) return hipErrorInvalidValue;
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, bool ec, hipStream_t stream) {
+    if (!big_supported(a, tile, flow, ec)) return hipErrorInvalidValue;
+    if (!ec)
+        return tile == SGEMM_EMU_TILE_128x128 ? launch_big_cfg<Big128x128NoEC>(a, stream)
+                                               : launch_big_cfg<Big128x256NoEC>(a, stream);
     if (flow == SGEMM_EMU_FLOW_DIRECT) return launch_big_cfg<Big128x128Direct>(a, stream);
     if (flow == SGEMM_EMU_FLOW_STAGED) return launch_big_cfg<Big128x128Staged>(a, stream);
     switch (tile) {

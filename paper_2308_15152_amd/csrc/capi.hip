@@ -157,12 +157,10 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
         // 8192^3 and on 256 x 1024 x 1024 x k for k >= 1024)
         const int order[3] = {wide ? SGEMM_EMU_TILE_128x256 : SGEMM_EMU_TILE_256x128,
                               SGEMM_EMU_TILE_256x128, SGEMM_EMU_TILE_128x128};
-        if (ec == 1) {
-            for (int t : order)
-                if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&
-                    sgemm_emu::big_supported(a, t, SGEMM_EMU_FLOW_SPLIT))
-                    big_tile = t;
-        }
+        for (int t : order)
+            if (big_tile == SGEMM_EMU_TILE_AUTO && (tile == SGEMM_EMU_TILE_AUTO || tile == t) &&
+                sgemm_emu::big_supported(a, t, SGEMM_EMU_FLOW_SPLIT, ec == 1))
+                big_tile = t;
         const double work = (double)batch * m * n * k;  // multiply-adds (no overflow)
         const double kDecompose = 34359738368.0;         // 2^35
         // the decomposition: whole tiles covering at least 95% of C, at least
@@ -214,7 +212,7 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
         kern = K_REG;
-    } else if (ec == 1 && sgemm_emu::big_supported(a, tile, flow)) {
+    } else if (sgemm_emu::big_supported(a, tile, flow, ec == 1)) {
         kern = K_BIG;  // full tiles: the pipelined kernel
     } else if (tile != SGEMM_EMU_TILE_128x256 && sgemm_emu::gemm_variant_exists(tile, flow)) {
         kern = K_LDS;
@@ -246,7 +244,7 @@ hipError_t run_tiled(const sgemm_emu::GemmArgs& a, int tile, hipStream_t stream)
     g.m = in.m;
     g.n = in.n;
     g.k = in.k;
-    hipError_t e = sgemm_emu::launch_gemm_big(g, tile, SGEMM_EMU_FLOW_SPLIT, stream);
+    hipError_t e = sgemm_emu::launch_gemm_big(g, tile, SGEMM_EMU_FLOW_SPLIT, true, stream);
     if (e != hipSuccess) return e;
     if (in.k < a.k) {
         sgemm_emu::AccArgs t{};
@@ -306,7 +304,7 @@ int run_gemm(int m, int n, int k, const float* A, int lda, const float* B, int l
     hipError_t e;
     switch (kern) {
         case K_REG: e = sgemm_emu::launch_gemm_reg(a, tile, ec != 0, stream); break;
-        case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, flow, stream); break;
+        case K_BIG: e = sgemm_emu::launch_gemm_big(a, tile, flow, ec != 0, stream); break;
         case K_TILED: e = run_tiled(a, tile, stream); break;
         default: e = sgemm_emu::launch_gemm(a, tile, flow, ec != 0, stream); break;
     }

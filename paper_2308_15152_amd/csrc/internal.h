@@ -32,11 +32,13 @@ bool reg_flow_supported(const GemmArgs& a, int tile);
 hipError_t launch_gemm_reg(const GemmArgs& a, int tile, bool ec, hipStream_t stream);
 
 // Pipelined full-tile kernels (split flow: tiles 128x128, 256x128,
-// 128x256; direct and staged flows: tile 128x128): true if the shape and
-// alignment allow the tile.
-bool big_supported(const GemmArgs& a, int tile, int flow);
-hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, hipStream_t stream);
-// True if launch_gemm_big runs the persistent stream form of the kernel.
+// 128x256; direct and staged flows: tile 128x128; error correction off:
+// split flow, tiles 128x128 and 128x256): true if the shape and alignment
+// allow the tile.
+bool big_supported(const GemmArgs& a, int tile, int flow, bool ec);
+hipError_t launch_gemm_big(const GemmArgs& a, int tile, int flow, bool ec, hipStream_t stream);
+// True if launch_gemm_big runs the persistent stream form of the kernel
+// (error correction on).
 bool big_streams(const GemmArgs& a, int tile, int flow);
 
 struct HouseholderArgs {

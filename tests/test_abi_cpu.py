@@ -228,10 +228,24 @@ def test_resolve_policy():
                                                     pkg.TILE_128x256))[0] == -8
     assert _resolve(128, 256, 64, policy=pkg.Policy(pkg.FLOW_DIRECT, 1,
                                                     pkg.TILE_128x256))[0] == -8
-    # without error correction the full-tile kernel is not used
+    # without error correction the full-tile kernel runs on its 128 x 128 and
+    # 128 x 256 tiles (split flow); other tiles and flows take the general kernel
     assert _resolve(256, 256, 256, policy=pkg.Policy(pkg.FLOW_SPLIT, 0,
                                                      pkg.TILE_256x128))[0] == 0
     assert _resolve.kernel == "bgemm_emu_kernel"
+    for tile in (pkg.TILE_128x128, pkg.TILE_128x256):
+        assert _resolve(256, 256, 256, policy=pkg.Policy(pkg.FLOW_SPLIT, 0, tile)) == (
+            0, (pkg.FLOW_SPLIT, 0, tile))
+        assert _resolve.kernel == "bgemm_big_kernel"
+    assert _resolve(256, 256, 256, policy=pkg.Policy(pkg.FLOW_DIRECT, 0, pkg.TILE_128x128))[0] == 0
+    assert _resolve.kernel == "bgemm_emu_kernel"
+    # AUTO tile without error correction: 128 x 256 for long k over much output, else 128 x 128
+    assert _resolve(8192, 8192, 8192, policy=pkg.Policy(pkg.FLOW_AUTO, 0, pkg.TILE_AUTO)) == (
+        0, (pkg.FLOW_SPLIT, 0, pkg.TILE_128x256))
+    assert _resolve.kernel == "bgemm_big_kernel"
+    assert _resolve(128, 128, 128, 4096, st=(128 * 128,) * 3,
+                    policy=pkg.Policy(pkg.FLOW_AUTO, 0, pkg.TILE_AUTO)) == (
+        0, (pkg.FLOW_SPLIT, 0, pkg.TILE_128x128))
     assert _resolve(-1, 4, 4)[0] == -1
     lib = pkg.load()
     assert lib.sgemm_emu_resolve_policy(4, 4, 4, ctypes.c_void_p(PA), 4, ctypes.c_void_p(PB), 4,

@@ -441,3 +441,26 @@ def test_register_flow_batch_past_one_launch():
     head = to_np(C[:P])
     gate(head, oracle.gemm(A.numpy(), B.numpy()), k, "register flow pool")
     assert_periodic(C, P, "register flow batch")
+
+
+@pytest.mark.parametrize("tile", [pkg.TILE_128x128, pkg.TILE_128x256])
+def test_full_tile_kernel_without_error_correction(tile):
+    """The full-tile kernel with error correction off (the measurement
+    variant of the hi.hi product alone) runs on both of its tiles: its result
+    is the product of the operands' hi parts up to FP32 accumulation, and its
+    error against the FP64 product is at the fp16 level."""
+    A, B = synth.gemm_inputs(2, 256, 512, 192, seed=23)
+    dev = device()
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.full((2, 256, 512), float("nan"), device=dev)
+    pol = pkg.Policy(pkg.FLOW_SPLIT, 0, tile)
+    _, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, C, policy=pol)
+    assert kern == "bgemm_big_kernel"
+    pkg.sgemm_emu_batched(Ad, Bd, C, policy=pol)
+    off = to_np(C)
+    ref = oracle.gemm(A.numpy(), B.numpy(), want=("c64", "n64"))
+    hiA = A.numpy().astype(np.float16).astype(np.float64)
+    hiB = B.numpy().astype(np.float16).astype(np.float64)
+    hh = np.einsum("bik,bkj->bij", hiA, hiB)
+    assert np.all(np.abs(off - hh) <= (192 + 2) * 2.0 ** -23 * ref["n64"])
+    assert oracle.max_rel_err(off, ref["c64"], ref["n64"]) > 2.0 ** -16
