@@ -329,9 +329,9 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: the emulated SGEMM is a single-GPU "
-              "library (batch sharding across GPUs needs no communication and is not "
-              "part of this build)", file=sys.stderr)
+        print("bench.py measures one GPU (--gpus 1): the library runs on a single GPU; "
+              "its batched workloads would shard by batch item with no communication, "
+              "so each GPU would run this same measurement on its share", file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
