@@ -25,8 +25,10 @@
  *   - Every argument is validated before anything is enqueued.  On an error
  *     nothing is launched and a negative code is returned; the functions
  *     never throw and never abort.
- *   - All functions are thread-safe: the library has no mutable global state
- *     except the last HIP error code, which is kept per thread.
+ *   - All functions are thread-safe: the library's only mutable global state
+ *     is the last HIP error code, kept per thread, and the number of
+ *     workgroups of a kernel that fit on a device, computed on first use and
+ *     kept in atomics.
  */
 #ifndef SGEMM_EMU_H
 #define SGEMM_EMU_H

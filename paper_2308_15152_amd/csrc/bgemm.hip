@@ -34,6 +34,7 @@
 // The transpose happens in registers during staging: a thread loads four
 // consecutive rows of four consecutive columns and writes each column's four
 // k values together.
+#include <atomic>
 #include <type_traits>
 
 #include "internal.h"
@@ -479,10 +480,17 @@ constexpr bool variant_fits() {
 // device of the calling thread is used).
 template <class CF>
 static int resident_blocks() {
-    static int cache[64] = {0};
+    // one value per device, computed on first use; atomic so that threads
+    // calling for the first time at once (all computing the same value) do
+    // not race; devices past the table are computed on every call
+    static std::atomic<int> cache[64];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cache[dev] > 0) return cache[dev];
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    const bool cached = dev < 64;
+    if (cached) {
+        const int r = cache[dev].load(std::memory_order_relaxed);
+        if (r > 0) return r;
+    }
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
@@ -490,7 +498,7 @@ static int resident_blocks() {
         hipSuccess)
         return 0;
     const int r = cus * (per_cu > 0 ? per_cu : 1);
-    cache[dev] = r;  // benign race: every thread computes the same value
+    if (cached) cache[dev].store(r, std::memory_order_relaxed);
     return r;
 }
 

@@ -55,6 +55,8 @@
 // Only full tiles (m and n multiples of the tile, k of 32) with 16-byte
 // aligned rows; other shapes take the general LDS kernel or the
 // register-direct flow.
+#include <atomic>
+
 #include "internal.h"
 #include "mfmae/frag.hpp"
 #include "mfmae/tcec.hpp"
@@ -745,17 +747,24 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_stream_kernel(BigPara
 // device).
 template <class CF, class K>
 int resident_wgs(K kernel) {
-    static int cache[64] = {0};
+    // one value per device, computed on first use; atomic so that threads
+    // calling for the first time at once (all computing the same value) do
+    // not race; devices past the table are computed on every call
+    static std::atomic<int> cache[64];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cache[dev] > 0) return cache[dev];
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    const bool cached = dev < 64;
+    if (cached) {
+        const int r = cache[dev].load(std::memory_order_relaxed);
+        if (r > 0) return r;
+    }
     int cus = 0, per_cu = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, CF::NT, 0) != hipSuccess)
         return 0;
     const int r = cus * (per_cu > 0 ? per_cu : 1);
-    cache[dev] = r;  // benign race: every thread computes the same value
+    if (cached) cache[dev].store(r, std::memory_order_relaxed);
     return r;
 }
 
