@@ -58,3 +58,48 @@ def test_operands_must_be_device_tensors():
         pkg.sgemm_emu_batched(A, torch.rand(2, 8, 8))
     with pytest.raises(ValueError):
         pkg.sgemm_emu_scan(torch.rand(4, 8))
+
+
+def test_calls_from_several_threads():
+    """The library's calls are thread-safe: four host threads, each on its own
+    stream (default priority), run products concurrently (the binding's
+    foreign calls release the interpreter lock) through three different
+    kernels; every result equals the same product run alone, bit for bit
+    (the kernels are deterministic)."""
+    import threading
+
+    import numpy as np
+
+    import synth
+    from gpu_util import to_np
+
+    dev = device()
+    shapes = [(64, 128, 128, 128), (2, 96, 80, 72), (3, 256, 256, 64), (5, 64, 64, 64)]
+    inputs = [tuple(t.to(dev) for t in synth.gemm_inputs(*s, seed=300 + i))
+              for i, s in enumerate(shapes)]
+    alone = [to_np(pkg.sgemm_emu_batched(A, B)) for A, B in inputs]
+    results = [[None] * 10 for _ in shapes]
+    errors = []
+
+    def work(i):
+        try:
+            A, B = inputs[i]
+            s = torch.cuda.Stream(device=dev)
+            with torch.cuda.stream(s):
+                for r in range(10):
+                    results[i][r] = pkg.sgemm_emu_batched(A, B)
+            s.synchronize()
+        except Exception as e:  # reported below, in the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(len(shapes))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    for i in range(len(shapes)):
+        for r in range(10):
+            got = to_np(results[i][r])
+            assert np.array_equal(got.view(np.uint32), alone[i].view(np.uint32)), (i, r)
