@@ -70,25 +70,26 @@ constexpr int kWaves = 4;  // waves (tasks) per workgroup
 // ---------------------------------------------------------------------------
 
 struct HouseholderRule {
-    const float* u;
+    // u arrives in one coalesced load, u_l in lane l; the entries the map
+    // asks for are read from the lane that holds them (cross-lane reads, no
+    // memory access), so building H adds no vector-memory instructions
+    float ulane;
     float urow[2];  // -2 u_i of the lane's row in each 32-row block
 
     __device__ void init(const RuleParams& p, int64_t item, unsigned char*) {
-        u = p.u + item * p.su;
+        ulane = p.u[item * p.su + (threadIdx.x & 63)];
         mfmae::foreach_ij<FragA>([&](int e, int i, int) {
             if (e == 0) {
-                urow[0] = -2.0f * u[i];
-                urow[1] = -2.0f * u[32 + i];
+                urow[0] = -2.0f * __shfl(ulane, i);
+                urow[1] = -2.0f * __shfl(ulane, 32 + i);
             }
         });
     }
 
     __device__ void build(int s, half8_t (&hh)[2], half8_t (&hl)[2]) const {
-        const int l = threadIdx.x & 63;
-        const float* us = u + 16 * s + 8 * (l >> 5);
         mfmae::foreach_ij<FragA>([&](int e, int i, int jj) {
             const int gj = 16 * s + jj;
-            const float uj = us[e];  // u[gj]: jj = 8 (l / 32) + e
+            const float uj = __shfl(ulane, gj);
 #pragma unroll
             for (int tm = 0; tm < 2; ++tm) {
                 const float h = __builtin_fmaf(urow[tm], uj, (32 * tm + i) == gj ? 1.0f : 0.0f);
@@ -232,17 +233,19 @@ struct HouseholderLdsRule : LdsOperand {
     __device__ void init(const RuleParams& p, int64_t item, unsigned char* lds) {
         const int l = threadIdx.x & 63;
         bind(lds);
-        const float* u = p.u + item * p.su;
+        // u as in the register-built rule: one coalesced load, entries read
+        // from the lane that holds them
+        const float ulane = p.u[item * p.su + l];
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const int piece = 64 * t + l;
             const int r = piece >> 3, q0 = 8 * (piece & 7);
-            const float ur = -2.0f * u[r];
+            const float ur = -2.0f * __shfl(ulane, r);
             float h[8];
 #pragma unroll
             for (int v = 0; v < 8; ++v)
                 h[v] = mfmae::tcec::as_fp32(
-                    __builtin_fmaf(ur, u[q0 + v], (r == q0 + v) ? 1.0f : 0.0f));
+                    __builtin_fmaf(ur, __shfl(ulane, q0 + v), (r == q0 + v) ? 1.0f : 0.0f));
             half8_t vh, vl;
             mfmae::tcec::split8(h, vh, vl);
             *reinterpret_cast<half8_t*>(hi + off(r, piece & 7)) = vh;
