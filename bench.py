@@ -210,6 +210,15 @@ def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO, hh_mode=pkg.HOUSEH
     return call, C
 
 
+def inputs_sha256(host_inputs) -> str:
+    """SHA-256 of the input tensors' bytes, in the order they are drawn (the
+    oracle and the device path see exactly these bytes)."""
+    h = hashlib.sha256()
+    for t in host_inputs:
+        h.update(t.contiguous().numpy().tobytes())
+    return h.hexdigest()
+
+
 def cpu_baseline(w, host_inputs, C_dev, target_s: float):
     """The oracle's plain FP32 product on a bounded sample of the workload,
     timed on the host cores; the same sample gives the accuracy of the GPU
@@ -438,6 +447,7 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         "data": "synthetic",
         "config": {"workload": w.name, "kind": w.kind, "batch": w.batch, "m": w.m, "n": w.n,
                    "k": w.k, "dist": w.dist, "seed": w.seed,
+                   "inputs_sha256": inputs_sha256(host_inputs),
                    "policy": None if resolved is None else
                    {"flow": resolved.flow, "ec": resolved.ec, "tile": resolved.tile,
                     "requested": "auto" if policy is None else "explicit"},
