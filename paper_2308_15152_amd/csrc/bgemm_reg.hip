@@ -195,7 +195,11 @@ struct RegParams {
 
 template <class CF>
 __global__ __launch_bounds__(CF::NT, CF::WAVES_PER_SIMD) void bgemm_reg_kernel(RegParams p) {
-    const int task = xcd_task(blockIdx.x, gridDim.x);
+    // Items of one tile share no operand: plain dispatch order (measured 5-7%
+    // faster than the XCD-aware numbering on 4096 x 128^3 with 128 x 128
+    // tiles); otherwise an item's tiles stay in one XCD's L2.
+    const int task =
+        p.tiles_m * p.tiles_n == 1 ? (int)blockIdx.x : xcd_task(blockIdx.x, gridDim.x);
     if (task >= p.ntasks) return;
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
