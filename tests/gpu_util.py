@@ -107,3 +107,13 @@ def assert_periodic(C: torch.Tensor, P: int, label: str = "", slab_items: int = 
             if not torch.equal(s[q * P:], head[:r]):
                 raise AssertionError(f"{label}: an item in [{t0 + q * P}, {t0 + s.shape[0]}) "
                                      f"differs from its pool item")
+
+
+def gate_repeated(C: torch.Tensor, ref: dict, P: int, items, k: int, label: str = ""):
+    """Element-wise bounds for chosen items of a periodic batch against the
+    oracle's results for the pool items they repeat (item t holds pool item
+    t mod P): the items on both sides of a launch boundary, say."""
+    items = sorted(set(int(t) for t in items))
+    got = to_np(C[items])
+    sub = {key: np.asarray(v)[[t % P for t in items]] for key, v in ref.items()}
+    return gate(got, sub, k, label, max_gate=False)

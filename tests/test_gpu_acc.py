@@ -22,7 +22,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
+from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -181,5 +181,8 @@ def test_batch_past_one_launch():
     Cd = periodic_batch(C.to(dev), batch)
     D = torch.full((batch, m, n), float("nan"), device=dev)
     pkg.sgemm_emu_batched_acc(Ad, Bd, Cd, D)
-    gate(to_np(D[:P]), oracle.gemm_acc(A.numpy(), B.numpy(), C.numpy()), k, "acc pool")
+    ref = oracle.gemm_acc(A.numpy(), B.numpy(), C.numpy())
+    gate(to_np(D[:P]), ref, k, "acc pool")
+    gate_repeated(D, ref, P, [per_launch - 1, per_launch, per_launch + 1, batch - 1], k,
+                  "acc, launch boundary")
     assert_periodic(D, P, "acc batch")

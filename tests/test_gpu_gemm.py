@@ -22,7 +22,8 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, gate_applies, periodic_batch, to_np
+from gpu_util import (assert_periodic, device, gate, gate_applies, gate_repeated, periodic_batch,
+                      to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -438,8 +439,10 @@ def test_register_flow_batch_past_one_launch():
     pol, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, C)
     assert kern == "bgemm_reg_kernel" and pol.tile == pkg.TILE_64x64, (pol, kern)
     pkg.sgemm_emu_batched(Ad, Bd, C)
-    head = to_np(C[:P])
-    gate(head, oracle.gemm(A.numpy(), B.numpy()), k, "register flow pool")
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    gate(to_np(C[:P]), ref, k, "register flow pool")
+    gate_repeated(C, ref, P, [per_launch - 1, per_launch, per_launch + 1, batch - 1], k,
+                  "register flow, launch boundary")
     assert_periodic(C, P, "register flow batch")
 
 

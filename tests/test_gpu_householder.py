@@ -20,7 +20,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
+from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -149,7 +149,10 @@ def test_batch_past_one_launch():
     Bd = periodic_batch(B.to(dev), batch)
     C = torch.full((batch, 64, ncols), float("nan"), device=dev)
     pkg.householder_emu_batched(ud, Bd, C)
-    gate(to_np(C[:P]), oracle.householder(u.numpy(), B.numpy()), 64, "householder pool")
+    ref = oracle.householder(u.numpy(), B.numpy())
+    gate(to_np(C[:P]), ref, 64, "householder pool")
+    gate_repeated(C, ref, P, [per_launch - 1, per_launch, per_launch + 1, batch - 1], 64,
+                  "householder, launch boundary")
     assert_periodic(C, P, "householder batch")
     del ud, Bd, C
     torch.cuda.empty_cache()

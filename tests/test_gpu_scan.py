@@ -28,7 +28,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, periodic_batch, to_np
+from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -124,7 +124,10 @@ def test_rows_past_one_launch():
     Xd = periodic_batch(X.to(device()), rows)
     Y = torch.full((rows, length), float("nan"), device=device())
     pkg.sgemm_emu_scan(Xd, Y)
-    gate(to_np(Y[:P]), oracle.scan(X.numpy()), _k_eff(length), "scan pool", max_gate=False)
+    ref = oracle.scan(X.numpy())
+    gate(to_np(Y[:P]), ref, _k_eff(length), "scan pool", max_gate=False)
+    gate_repeated(Y, ref, P, [per_launch - 1, per_launch, per_launch + 1, rows - 1],
+                  _k_eff(length), "scan, launch boundary")
     assert_periodic(Y, P, "scan rows")
     del Xd, Y
     torch.cuda.empty_cache()
