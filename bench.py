@@ -145,6 +145,10 @@ def parse():
     ap.add_argument("--batch", type=int, default=None,
                     help="override the workload's batch size (a measurement variant, "
                          "recorded in config; the default line uses the workload's own)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the K timed steps in one HIP graph (torch.cuda.CUDAGraph) "
+                         "and time one replay of it: per-step time without the host's "
+                         "launch overhead, for launch-bound workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target host time of the CPU-baseline sample")
@@ -377,13 +381,34 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
     for _ in range(args.warmup):
         call()
     torch.cuda.synchronize()
+    launches = args.steps  # host calls in the timed region
+    if args.graph:
+        # the K steps captured in one graph on a side stream (default
+        # priority) and replayed once: one graph launch per K steps instead
+        # of K kernel launches (a graph launch costs more than a kernel
+        # launch, so a graph of one step would be slower).  The library
+        # launches on the capturing stream and allocates nothing, so the
+        # graph holds the steps' kernels only.
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(graph, stream=side):
+                for _ in range(args.steps):
+                    call()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        call = graph.replay
+        launches = 1
+        call()  # one untimed replay
+        torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
+    for _ in range(launches):
         call()
     ev1.record(stream)
     torch.cuda.synchronize()
@@ -448,6 +473,7 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         "config": {"workload": w.name, "kind": w.kind, "batch": w.batch, "m": w.m, "n": w.n,
                    "k": w.k, "dist": w.dist, "seed": w.seed,
                    "inputs_sha256": inputs_sha256(host_inputs),
+                   "graph": bool(args.graph),
                    "policy": None if resolved is None else
                    {"flow": resolved.flow, "ec": resolved.ec, "tile": resolved.tile,
                     "requested": "auto" if policy is None else "explicit"},
