@@ -25,6 +25,9 @@
  *   - Every argument is validated before anything is enqueued.  On an error
  *     nothing is launched and a negative code is returned; the functions
  *     never throw and never abort.
+ *   - Calls may be captured in a HIP graph (stream capture): a call only
+ *     launches kernels on the given stream; it allocates nothing, records no
+ *     memset and does not synchronize.
  *   - All functions are thread-safe: the library's only mutable global state
  *     is the last HIP error code, kept per thread, and the number of
  *     workgroups of a kernel that fit on a device, computed on first use and
