@@ -8,6 +8,7 @@
 """
 import ctypes
 import os
+import pathlib
 import re
 import subprocess
 
@@ -480,3 +481,25 @@ def test_map_rejects_out_of_range():
     assert lib.mfmae_num_elements(0, 5) == -6
     ii = (ctypes.c_int * 16)()
     assert lib.mfmae_foreach(0, 0, 64, ii, ii) == -1
+
+
+def test_header_constants_match_binding():
+    """Every value constant of the C header (policy flows and tiles, operand
+    layouts, modes, MFMA shapes and uses) has the same value in the Python
+    binding, under the header's name without its prefix; error codes match
+    the library's own strerror table."""
+    text = pathlib.Path(pkg.__file__).resolve().parents[1].joinpath(
+        "include", "sgemm_emu.h").read_text()
+    consts = {m.group(1): int(m.group(2)) for m in re.finditer(
+        r"^#define\s+((?:SGEMM_EMU|MFMAE)_\w+)\s+\(?(-?\d+)\)?", text, flags=re.M)}
+    assert len(consts) >= 30
+    for name, value in consts.items():
+        short = re.sub(r"^(SGEMM_EMU|MFMAE)_", "", name)
+        if short == "OK" or short.startswith("ERR_"):
+            assert value <= 0
+            continue
+        assert getattr(pkg, short) == value, name
+    codes = sorted(v for k, v in consts.items() if k.startswith("SGEMM_EMU_ERR_"))
+    assert codes == list(range(-8, 0))
+    for code in codes:
+        assert "unknown" not in pkg.sgemm_emu_strerror(code)
