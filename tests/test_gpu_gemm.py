@@ -467,3 +467,33 @@ def test_full_tile_kernel_without_error_correction(tile):
     hh = np.einsum("bik,bkj->bij", hiA, hiB)
     assert np.all(np.abs(off - hh) <= (192 + 2) * 2.0 ** -23 * ref["n64"])
     assert oracle.max_rel_err(off, ref["c64"], ref["n64"]) > 2.0 ** -16
+
+
+def _random_shapes(n, seed):
+    g = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        out.append((int(g.integers(1, 4)), int(g.integers(1, 300)), int(g.integers(1, 300)),
+                    int(g.integers(1, 400))))
+    return out
+
+
+RANDOM_SHAPES = _random_shapes(12, 2024)
+
+
+@pytest.mark.parametrize("shape", RANDOM_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_random_shapes_every_policy(shape):
+    """Seeded random ragged shapes (batch 1-3, m and n 1-299, k 1-399) on the
+    automatic policy and every explicit policy that accepts them."""
+    batch, m, n, k = shape
+    print(f"case random {shape}", flush=True)
+    A, B = synth.gemm_inputs(batch, m, n, k, seed=7 * m + 3 * n + k)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    for policy in [None] + POLICIES:
+        if not _reg_supported(policy, k, n):
+            continue
+        if policy is not None and policy.tile == pkg.TILE_128x256:
+            continue
+        C = _run(A, B, policy)
+        gate(C, ref, k, f"{shape} {_pid(policy) if policy else 'auto'}",
+             max_gate=gate_applies(k, batch * m * n))
