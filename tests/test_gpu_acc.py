@@ -22,7 +22,8 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
+from gpu_util import (assert_periodic, device, gate, gate_applies, gate_repeated, periodic_batch,
+                      to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -186,3 +187,24 @@ def test_batch_past_one_launch():
     gate_repeated(D, ref, P, [per_launch - 1, per_launch, per_launch + 1, batch - 1], k,
                   "acc, launch boundary")
     assert_periodic(D, P, "acc batch")
+
+
+def _random_shapes(n, seed):
+    g = np.random.default_rng(seed)
+    return [(int(g.integers(1, 4)), int(g.integers(1, 200)), int(g.integers(1, 200)),
+             int(g.integers(0, 300))) for _ in range(n)]
+
+
+@pytest.mark.parametrize("shape", _random_shapes(8, 4048), ids=lambda s: "x".join(map(str, s)))
+def test_random_shapes_all_layouts(shape):
+    """Seeded random ragged shapes (k = 0 included in the range) under every
+    combination of instruction shape, transposes and C/D layout."""
+    batch, m, n, k = shape
+    print(f"case acc random {shape}", flush=True)
+    A, B, C = _draw(batch, m, n, k, seed=11 * m + n + 3 * k)
+    ref = oracle.gemm_acc(A.numpy(), B.numpy(), C.numpy())
+    for combo in COMBOS:
+        s, oa, ob, lay = combo
+        D = _run(A, B, C, oa, ob, lay, SHAPES[s])
+        gate(D, ref, max(k, 1), f"acc random {shape} {_cid(combo)}",
+             max_gate=gate_applies(k, batch * m * n))
