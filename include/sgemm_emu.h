@@ -135,7 +135,12 @@ int sgemm_emu_batched(int m, int n, int k,
  *                         Otherwise SGEMM_EMU_ERR_POLICY.
  * ec:   1 = error correction (3 products), 0 = hi.hi only (the comparison
  *       without correction: accuracy and cost).
- * tile: 0 = automatic, or one of SGEMM_EMU_TILE_*.
+ * tile: 0 = automatic, or one of SGEMM_EMU_TILE_*.  With flow AUTO the
+ *       tile follows the flow the library picks.  With a named flow, AUTO
+ *       picks a tile that flow has: REG 64x64 when m, n <= 64, else 128x128
+ *       where its B vectors allow it, else 64x64; DIRECT and STAGED 64x64
+ *       when m, n <= 64, else 128x128; SPLIT by shape (64x64 when m, n <= 64,
+ *       256x128 for many 256-row tiles, else 128x128).
  */
 #define SGEMM_EMU_FLOW_AUTO 0
 #define SGEMM_EMU_FLOW_SPLIT 1
@@ -193,6 +198,31 @@ int sgemm_emu_resolve_policy(int m, int n, int k,
                              const sgemm_emu_policy_t* policy,
                              sgemm_emu_policy_t* out,
                              const char** kernel);
+
+/*
+ * Work distribution of the GEMM kernels, computed on the host by the same
+ * functions the kernels run (no GPU is touched): which task each workgroup
+ * takes and which tile of an item each task is.  These decide that every
+ * output tile is computed exactly once, so they are exposed to be checked.
+ *
+ * sgemm_emu_xcd_order: task_of_workgroup[b] for b in [0, grid) is the task
+ *   workgroup b of a grid of `grid` workgroups takes first (the full-tile
+ *   and register-flow kernels take only that task; the persistent kernels
+ *   take it and every grid-th task after it).  Workgroups are dispatched
+ *   round-robin over the 8 XCDs; the numbering gives each XCD one contiguous
+ *   range of task ids.  grid >= 1; task_of_workgroup holds grid ints
+ *   (caller-owned host memory).
+ * sgemm_emu_tile_order: for task t in [0, tiles_m * tiles_n) of one batch
+ *   item, tile_row[t] and tile_col[t] are the tile's row and column in the
+ *   tiles_m x tiles_n grid of output tiles (groups of 8 tile rows, column by
+ *   column within a group).  tiles_m, tiles_n >= 1 and their product below
+ *   2^31; each array holds tiles_m * tiles_n ints (caller-owned host
+ *   memory).
+ * Both return SGEMM_EMU_OK, SGEMM_EMU_ERR_DIM for sizes out of range, or
+ * SGEMM_EMU_ERR_NULL for a NULL array.
+ */
+int sgemm_emu_xcd_order(int grid, int* task_of_workgroup);
+int sgemm_emu_tile_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col);
 
 /*
  * Batched multiply-accumulate in emulated FP32 with transposable operands:
@@ -341,10 +371,28 @@ int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx,
  * device: hi[i], lo[i] receive the binary16 bit patterns of
  * toFP16(x[i]) and toFP16((x[i] - toFP32(hi)) * 2^11).  count >= 0; x, hi
  * and lo are device pointers of count elements and must not overlap.
- * Errors: SGEMM_EMU_ERR_DIM (also when count elements run past the end of
- * the address space), _NULL, _ALIAS, _HIP.
+ * form selects the device function that splits, so that each form the
+ * kernels use can be checked bit for bit:
+ *   SGEMM_EMU_SPLIT_SCALAR  one value at a time (rule-built entries, the
+ *                           B operand of the Householder and Givens
+ *                           kernels, single values at tile edges)
+ *   SGEMM_EMU_SPLIT_PAIR    two values at a time, hi converted as a packed
+ *                           pair (B staging of the full-tile kernel, the
+ *                           general kernel's staging)
+ *   SGEMM_EMU_SPLIT_EIGHT   eight consecutive values into one operand vector
+ *                           (A staging of the full-tile kernel, the per-wave
+ *                           split of the direct and staged flows, the
+ *                           register-direct flow, the fragment loads, the
+ *                           scan, the Householder baseline's entries)
+ * Values past the last whole pair or group of eight are split one at a
+ * time.  Errors: SGEMM_EMU_ERR_DIM (also when count elements run past the
+ * end of the address space), _NULL, _ALIAS, SGEMM_EMU_ERR_POLICY (form
+ * unknown), _HIP.
  */
-int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+#define SGEMM_EMU_SPLIT_SCALAR 0
+#define SGEMM_EMU_SPLIT_PAIR 1
+#define SGEMM_EMU_SPLIT_EIGHT 2
+int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo, int form,
                     hipStream_t stream);
 
 /* ---- Fragment maps (Sec. 2.3.2, 4.2, 4.3) ------------------------------

@@ -24,7 +24,8 @@ __all__ = [
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
-    "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order",
+    "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS", "SPLIT_SCALAR", "SPLIT_PAIR", "SPLIT_EIGHT",
     "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
     "Policy", "FLOW_AUTO", "FLOW_SPLIT", "FLOW_DIRECT", "FLOW_STAGED", "FLOW_REG",
@@ -43,6 +44,7 @@ USE_A, USE_B, USE_ACC = 0, 1, 2
 GIVENS_AUTO, GIVENS_MAP, GIVENS_EMBEDDED, GIVENS_LDS = 0, 1, 2, 3
 OP_N, OP_T = 0, 1
 HOUSEHOLDER_RULE, HOUSEHOLDER_LDS = 0, 1
+SPLIT_SCALAR, SPLIT_PAIR, SPLIT_EIGHT = 0, 1, 2
 ROW_MAJOR, COL_MAJOR = 0, 1
 
 # Every symbol declared in include/sgemm_emu.h.
@@ -52,6 +54,7 @@ EXPORTED_SYMBOLS = (
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order",
 )
 
 
@@ -117,13 +120,15 @@ def load():
                                        i32),
         "givens_emu_batched": ([i32, i32, i32, P, P, i64, P, i32, i64, i32, P, i32, i64, i32,
                                 i32, P], i32),
-        "sgemm_emu_split": ([i64, P, P, P, P], i32),
+        "sgemm_emu_split": ([i64, P, P, P, i32, P], i32),
         "mfmae_num_elements": ([i32, i32], i32),
         "mfmae_map": ([i32, i32, i32, i32, ip, ip], i32),
         "mfmae_foreach": ([i32, i32, i32, ip, ip], i32),
         "mfmae_mma_probe": ([i32, P, P, P, P], i32),
         "sgemm_emu_strerror": ([i32], ctypes.c_char_p),
         "sgemm_emu_last_hip_error": ([], i32),
+        "sgemm_emu_xcd_order": ([i32, P], i32),
+        "sgemm_emu_tile_order": ([i32, i32, P, P], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -274,6 +279,34 @@ def sgemm_emu_resolve_policy(A, B, C, *, policy: Policy | None = None):
     return out, (kern.value or b"").decode()
 
 
+def sgemm_emu_xcd_order(grid: int):
+    """Task each workgroup of a grid of ``grid`` workgroups takes first (the
+    kernels' XCD-aware numbering, computed on the host), as a numpy int32
+    array of ``grid`` entries."""
+    import numpy as np
+
+    out = np.empty(max(int(grid), 0), dtype=np.int32)
+    _check(load().sgemm_emu_xcd_order(int(grid), out.ctypes.data_as(ctypes.c_void_p)),
+           "sgemm_emu_xcd_order")
+    return out
+
+
+def sgemm_emu_tile_order(tiles_m: int, tiles_n: int):
+    """(tile row, tile column) of each task of one item, in task order (the
+    kernels' grouped tile order, computed on the host): two numpy int32
+    arrays of ``tiles_m * tiles_n`` entries."""
+    import numpy as np
+
+    count = max(int(tiles_m), 0) * max(int(tiles_n), 0)
+    rows = np.empty(count, dtype=np.int32)
+    cols = np.empty(count, dtype=np.int32)
+    _check(load().sgemm_emu_tile_order(int(tiles_m), int(tiles_n),
+                                       rows.ctypes.data_as(ctypes.c_void_p),
+                                       cols.ctypes.data_as(ctypes.c_void_p)),
+           "sgemm_emu_tile_order")
+    return rows, cols
+
+
 def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):
     return sgemm_emu_batched(A, B, C, policy=policy, stream=stream)
 
@@ -421,9 +454,10 @@ def givens_emu_batched(i, j, c, s, B, C=None, *, mode: int = GIVENS_AUTO, stream
     return C
 
 
-def sgemm_emu_split(x, *, stream=None):
+def sgemm_emu_split(x, *, form: int = SPLIT_SCALAR, stream=None):
     """Elementwise split on the device: (hi, lo) binary16 bit patterns as int16
-    tensors of x's shape (x: contiguous float32 device tensor)."""
+    tensors of x's shape (x: contiguous float32 device tensor).  ``form``
+    picks the device function: SPLIT_SCALAR, SPLIT_PAIR or SPLIT_EIGHT."""
     import torch
 
     if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
@@ -431,7 +465,8 @@ def sgemm_emu_split(x, *, stream=None):
     hi = torch.empty(x.shape, dtype=torch.int16, device=x.device)
     lo = torch.empty(x.shape, dtype=torch.int16, device=x.device)
     with _on_device(x, hi, lo):
-        rc = load().sgemm_emu_split(x.numel(), _ptr(x), _ptr(hi), _ptr(lo), _stream(stream))
+        rc = load().sgemm_emu_split(x.numel(), _ptr(x), _ptr(hi), _ptr(lo), int(form),
+                                    _stream(stream))
     _check(rc, "sgemm_emu_split")
     return hi, lo
 

@@ -538,7 +538,6 @@ static hipError_t launch_cfg(const GemmArgs& a, hipStream_t stream) {
         if (blocks >= 8) blocks -= blocks % 8;
         p.ntasks = (int)ntasks;
         p.item0 = (int)i0;
-        p.xcd_remap = (blocks % 8 == 0) ? 1 : 0;
         hipLaunchKernelGGL(bgemm_emu_kernel<CF>, dim3((unsigned)blocks), dim3(CF::NT), 0, stream, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -455,17 +455,9 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
     if (task >= p.ntasks) return;  // the whole workgroup leaves together
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
-    const int t = task - item * tiles;
-    // tiles in groups of 8 tile rows, so that the workgroups running at the
-    // same time on one XCD share B columns
-    constexpr int GROUP_M = 8;
-    const int group_size = GROUP_M * p.tiles_n;
-    const int grp = t / group_size;
-    const int first_m = grp * GROUP_M;
-    const int gm = min(p.tiles_m - first_m, GROUP_M);
-    const int r = t - grp * group_size;
-    const int m0 = (first_m + r % gm) * CF::BM;
-    const int n0 = (r / gm) * CF::BN;
+    const TileRC rc = grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
+    const int m0 = rc.tm * CF::BM;
+    const int n0 = rc.tn * CF::BN;
 
     const int64_t it = (int64_t)item + p.item0;
     const float* __restrict__ Ab = p.A + it * p.sa;
@@ -575,22 +567,14 @@ template <class CF>
 __device__ inline TaskGeo task_geo(const BigParams& p, int task) {
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
-    const int t = task - item * tiles;
-    // tiles in groups of 8 tile rows, so that the workgroups running at the
-    // same time on one XCD share B columns
-    constexpr int GROUP_M = 8;
-    const int group_size = GROUP_M * p.tiles_n;
-    const int grp = t / group_size;
-    const int first_m = grp * GROUP_M;
-    const int gm = min(p.tiles_m - first_m, GROUP_M);
-    const int r = t - grp * group_size;
+    const TileRC rc = grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
     TaskGeo q;
     const int64_t it = (int64_t)item + p.item0;
     q.A = p.A + it * p.sa;
     q.B = p.B + it * p.sb;
     q.C = p.C + it * p.sc;
-    q.m0 = (first_m + r % gm) * CF::BM;
-    q.n0 = (r / gm) * CF::BN;
+    q.m0 = rc.tm * CF::BM;
+    q.n0 = rc.tn * CF::BN;
     return q;
 }
 

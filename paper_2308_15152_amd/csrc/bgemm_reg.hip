@@ -203,17 +203,9 @@ __global__ __launch_bounds__(CF::NT, CF::WAVES_PER_SIMD) void bgemm_reg_kernel(R
     if (task >= p.ntasks) return;
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
-    const int t = task - item * tiles;
-    // tiles in groups of 8 tile rows, so that the workgroups running at the
-    // same time on one XCD share B columns as well as A rows
-    constexpr int GROUP_M = 8;
-    const int group_size = GROUP_M * p.tiles_n;
-    const int grp = t / group_size;
-    const int first_m = grp * GROUP_M;
-    const int gm = min(p.tiles_m - first_m, GROUP_M);
-    const int r = t - grp * group_size;
-    const int tile_m = first_m + r % gm;
-    const int tile_n = r / gm;
+    const TileRC rc = grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
+    const int tile_m = rc.tm;
+    const int tile_n = rc.tn;
 
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int l = threadIdx.x & 63;

@@ -8,6 +8,7 @@
 #include "internal.h"
 #include "mfmae/frag.hpp"
 #include "sgemm_emu.h"
+#include "tiling.hpp"
 
 namespace {
 
@@ -59,6 +60,27 @@ int pick_tile(int m, int n, int batch) {
     const int64_t big = (int64_t)((m + 255) / 256) * ((n + 127) / 128) * batch;
     if (m >= 256 && big >= 1024) return SGEMM_EMU_TILE_256x128;
     return SGEMM_EMU_TILE_128x128;
+}
+
+// AUTO tile under a flow the caller named: a tile that flow is built for.
+// The register-direct flow has 64x64 and 128x128 tiles (128x128 only when
+// B's rows allow its vector loads); the direct and staged flows run on
+// 64x64 and 128x128 everywhere (the full-tile kernel has them on 128x128
+// only, the staged flow's general kernel stops at 128x128).  The split flow
+// takes the shape-based choice.
+int pick_tile_for_flow(const sgemm_emu::GemmArgs& a, int flow, int batch) {
+    const bool small = a.m <= 64 && a.n <= 64;
+    switch (flow) {
+        case SGEMM_EMU_FLOW_REG:
+            if (small) return SGEMM_EMU_TILE_64x64;
+            return sgemm_emu::reg_flow_supported(a, SGEMM_EMU_TILE_128x128)
+                       ? SGEMM_EMU_TILE_128x128
+                       : SGEMM_EMU_TILE_64x64;
+        case SGEMM_EMU_FLOW_DIRECT:
+        case SGEMM_EMU_FLOW_STAGED:
+            return small ? SGEMM_EMU_TILE_64x64 : SGEMM_EMU_TILE_128x128;
+        default: return pick_tile(a.m, a.n, batch);
+    }
 }
 
 // Validation shared by the two GEMM entry points.
@@ -208,7 +230,7 @@ int resolve_gemm(int m, int n, int k, const float* A, int lda, const float* B, i
             flow = SGEMM_EMU_FLOW_SPLIT;
         }
     }
-    if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile(m, n, batch);
+    if (tile == SGEMM_EMU_TILE_AUTO) tile = pick_tile_for_flow(a, flow, batch);
     if (flow == SGEMM_EMU_FLOW_REG) {
         if (!sgemm_emu::reg_flow_supported(a, tile)) return SGEMM_EMU_ERR_POLICY;
         kern = K_REG;
@@ -395,6 +417,26 @@ int sgemm_emu_resolve_policy(int m, int n, int k, const float* A, int lda, const
     return SGEMM_EMU_OK;
 }
 
+int sgemm_emu_xcd_order(int grid, int* task_of_workgroup) {
+    if (grid < 1) return SGEMM_EMU_ERR_DIM;
+    if (task_of_workgroup == nullptr) return SGEMM_EMU_ERR_NULL;
+    for (int b = 0; b < grid; ++b) task_of_workgroup[b] = sgemm_emu::xcd_task(b, grid);
+    return SGEMM_EMU_OK;
+}
+
+int sgemm_emu_tile_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col) {
+    if (tiles_m < 1 || tiles_n < 1 || (int64_t)tiles_m * tiles_n > INT32_MAX)
+        return SGEMM_EMU_ERR_DIM;
+    if (tile_row == nullptr || tile_col == nullptr) return SGEMM_EMU_ERR_NULL;
+    const int tiles = tiles_m * tiles_n;
+    for (int t = 0; t < tiles; ++t) {
+        const sgemm_emu::TileRC rc = sgemm_emu::grouped_tile(t, tiles_m, tiles_n);
+        tile_row[t] = rc.tm;
+        tile_col[t] = rc.tn;
+    }
+    return SGEMM_EMU_OK;
+}
+
 int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k, const float* A,
                           int lda, const float* B, int ldb, const float* C, int ldc, float* D,
                           int ldd, int batch, sgemm_emu_stride4_t stride, int shape, int ec,
@@ -573,9 +615,10 @@ int sgemm_emu_scan(int64_t rows, int len, const float* X, int64_t ldx, float* Y,
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
-int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo, int form,
                     hipStream_t stream) {
     if (count < 0) return SGEMM_EMU_ERR_DIM;
+    if (form < SGEMM_EMU_SPLIT_SCALAR || form > SGEMM_EMU_SPLIT_EIGHT) return SGEMM_EMU_ERR_POLICY;
     if (count == 0) return SGEMM_EMU_OK;
     if (x == nullptr || hi == nullptr || lo == nullptr) return SGEMM_EMU_ERR_NULL;
     const Extent ex = extent(x, 1, 1, count, count, 0, 4);
@@ -583,7 +626,7 @@ int sgemm_emu_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
     const Extent el = extent(lo, 1, 1, count, count, 0, 2);
     if (!all_ok({ex, eh, el})) return SGEMM_EMU_ERR_DIM;
     if (overlap(ex, eh) || overlap(ex, el) || overlap(eh, el)) return SGEMM_EMU_ERR_ALIAS;
-    hipError_t e = sgemm_emu::launch_split(count, x, hi, lo, stream);
+    hipError_t e = sgemm_emu::launch_split(count, x, hi, lo, form, stream);
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 

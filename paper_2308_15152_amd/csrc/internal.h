@@ -105,7 +105,8 @@ struct ScanArgs {
 
 hipError_t launch_scan(const ScanArgs& a, hipStream_t stream);
 
-hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+// form: SGEMM_EMU_SPLIT_SCALAR, _PAIR or _EIGHT.
+hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo, int form,
                         hipStream_t stream);
 
 hipError_t launch_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,

@@ -22,7 +22,6 @@ struct KParams {
     int ntasks;       // (items of this launch) x (tiles per item)
     int item0;        // first batch item of this launch
     int vec_a, vec_b;
-    int xcd_remap;    // 1 if gridDim.x is a multiple of 8
 };
 
 // ---------------------------------------------------------------------------
@@ -41,25 +40,42 @@ struct KParams {
 // are ordered in groups of GROUP_M tile rows so that consecutive tiles reuse
 // the same B columns.
 // ---------------------------------------------------------------------------
-__device__ inline int first_task(const KParams& p) {
-    int b = blockIdx.x;
-    if (p.xcd_remap) {
-        const int per = gridDim.x >> 3;
-        b = (b & 7) * per + (b >> 3);
-    }
-    return b;
-}
 
 // Task of workgroup b in a grid of G workgroups.  Workgroups are dispatched
 // round-robin over the 8 XCDs, so b runs on XCD b % 8 as that XCD's
 // (b / 8)-th workgroup; numbering them so that every XCD receives one
 // contiguous range of task ids keeps the tiles of one item, which share A
-// rows and B columns, in one L2.  A bijection of [0, G) for any G.
-__device__ inline int xcd_task(int b, int G) {
+// rows and B columns, in one L2.  A bijection of [0, G) for any G >= 1: XCD
+// x < G mod 8 receives floor(G / 8) + 1 ids, the others floor(G / 8).
+__host__ __device__ inline int xcd_task(int b, int G) {
     const int x = b & 7, i = b >> 3;
     const int q = G >> 3, r = G & 7;
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
+
+// Tile (row, column) of the t-th task of one item in a grid of tiles_m x
+// tiles_n tiles.  Tiles are taken in groups of GROUP_M tile rows (the last
+// group may hold fewer), column by column within a group, so that the
+// workgroups running at the same time on one XCD share B columns as well as
+// A rows.  A bijection of [0, tiles_m tiles_n) onto the tile grid.
+constexpr int GROUP_M = 8;
+
+struct TileRC {
+    int tm, tn;
+};
+
+__host__ __device__ inline TileRC grouped_tile(int t, int tiles_m, int tiles_n) {
+    const int group_size = GROUP_M * tiles_n;
+    const int grp = t / group_size;
+    const int first_m = grp * GROUP_M;
+    const int rest = tiles_m - first_m;
+    const int gm = rest < GROUP_M ? rest : GROUP_M;
+    const int r = t - grp * group_size;
+    return {first_m + r % gm, r / gm};
+}
+
+// The persistent kernels: workgroup b of G walks tasks xcd_task(b, G) + i G.
+__device__ inline int first_task(const KParams& p) { return xcd_task(blockIdx.x, gridDim.x); }
 
 struct TaskPos {
     const float* A;  // item base pointers
@@ -72,20 +88,14 @@ template <int BM, int BN>
 __device__ inline TaskPos task_pos(const KParams& p, int task) {
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
-    const int t = task - item * tiles;
-    constexpr int GROUP_M = 8;
-    const int group_size = GROUP_M * p.tiles_n;
-    const int g = t / group_size;
-    const int first_m = g * GROUP_M;
-    const int gm = min(p.tiles_m - first_m, GROUP_M);
-    const int r = t - g * group_size;
+    const TileRC rc = grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
     const int64_t it = (int64_t)item + p.item0;
     TaskPos q;
     q.A = p.A + it * p.sa;
     q.B = p.B + it * p.sb;
     q.C = p.C + it * p.sc;
-    q.m0 = (first_m + r % gm) * BM;
-    q.n0 = (r / gm) * BN;
+    q.m0 = rc.tm * BM;
+    q.n0 = rc.tn * BN;
     return q;
 }
 

@@ -9,24 +9,65 @@
 
 namespace sgemm_emu {
 
+// Each thread splits one group of 8 consecutive values with the chosen
+// device function; a group cut short by the end of x is split one value at
+// a time.
+template <int FORM>
 __global__ __launch_bounds__(256) void split_kernel(int64_t count, const float* __restrict__ x,
                                                     uint16_t* __restrict__ hi,
                                                     uint16_t* __restrict__ lo) {
+    const int64_t groups = (count + 7) / 8;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) {
-        _Float16 h, l;
-        mfmae::tcec::split(x[i], h, l);
-        hi[i] = __builtin_bit_cast(uint16_t, h);
-        lo[i] = __builtin_bit_cast(uint16_t, l);
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < groups; g += stride) {
+        const int64_t i0 = 8 * g;
+        if (FORM != SGEMM_EMU_SPLIT_SCALAR && i0 + 8 <= count) {
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = x[i0 + e];
+            if constexpr (FORM == SGEMM_EMU_SPLIT_EIGHT) {
+                mfmae::half8_t h, l;
+                mfmae::tcec::split8(v, h, l);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    hi[i0 + e] = __builtin_bit_cast(uint16_t, h[e]);
+                    lo[i0 + e] = __builtin_bit_cast(uint16_t, l[e]);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    mfmae::tcec::half2_t h, l;
+                    mfmae::tcec::split_pair(v[e], v[e + 1], h, l);
+                    hi[i0 + e] = __builtin_bit_cast(uint16_t, h[0]);
+                    hi[i0 + e + 1] = __builtin_bit_cast(uint16_t, h[1]);
+                    lo[i0 + e] = __builtin_bit_cast(uint16_t, l[0]);
+                    lo[i0 + e + 1] = __builtin_bit_cast(uint16_t, l[1]);
+                }
+            }
+            continue;
+        }
+        for (int64_t i = i0; i < count && i < i0 + 8; ++i) {
+            _Float16 h, l;
+            mfmae::tcec::split(x[i], h, l);
+            hi[i] = __builtin_bit_cast(uint16_t, h);
+            lo[i] = __builtin_bit_cast(uint16_t, l);
+        }
     }
 }
 
-hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo,
+hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo, int form,
                         hipStream_t stream) {
     if (count == 0) return hipSuccess;
-    int64_t blocks = (count + 255) / 256;
+    int64_t blocks = ((count + 7) / 8 + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(split_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, count, x, hi, lo);
+    if (form == SGEMM_EMU_SPLIT_EIGHT)
+        hipLaunchKernelGGL(split_kernel<SGEMM_EMU_SPLIT_EIGHT>, dim3((unsigned)blocks), dim3(256),
+                           0, stream, count, x, hi, lo);
+    else if (form == SGEMM_EMU_SPLIT_PAIR)
+        hipLaunchKernelGGL(split_kernel<SGEMM_EMU_SPLIT_PAIR>, dim3((unsigned)blocks), dim3(256),
+                           0, stream, count, x, hi, lo);
+    else
+        hipLaunchKernelGGL(split_kernel<SGEMM_EMU_SPLIT_SCALAR>, dim3((unsigned)blocks),
+                           dim3(256), 0, stream, count, x, hi, lo);
     return hipGetLastError();
 }
 

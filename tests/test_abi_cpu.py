@@ -157,11 +157,11 @@ def test_resolve_policy():
     assert _resolve.kernel == "bgemm_big_kernel"
     # the batched experiment of Sec. 4.4.2: 128x256 from k = 1024 on
     s1m = 1024 * 1024
-    far = dict(A=1 << 40, B=2 << 40, C=3 << 40)  # gigabytes apart: no overlap
+    apart = dict(A=1 << 40, B=2 << 40, C=3 << 40)  # gigabytes apart: no overlap
     assert _resolve(1024, 1024, 512, 256, (1024 * 512, 512 * 1024, s1m),
-                    **far) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
+                    **apart) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_256x128))
     assert _resolve(1024, 1024, 1024, 256, (s1m, s1m, s1m),
-                    **far) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
+                    **apart) == (0, (pkg.FLOW_SPLIT, 1, pkg.TILE_128x256))
     assert _resolve(64, 64, 64, 16, (4096, 4096, 4096)) == (0, (pkg.FLOW_REG, 1,
                                                                  pkg.TILE_64x64))
     assert _resolve.kernel == "bgemm_reg_kernel"
@@ -248,6 +248,28 @@ def test_resolve_policy():
                     policy=pkg.Policy(pkg.FLOW_AUTO, 0, pkg.TILE_AUTO)) == (
         0, (pkg.FLOW_SPLIT, 0, pkg.TILE_128x128))
     assert _resolve(-1, 4, 4)[0] == -1
+    # a named flow with AUTO tile takes a tile that flow is built for (256^3 x
+    # 1024 would pick 256x128 by shape, which REG and STAGED do not have)
+    s256 = 256 * 256
+    auto_cases = [
+        ((256, 256, 256, 1024, (s256,) * 3), pkg.FLOW_REG, pkg.TILE_128x128, "bgemm_reg_kernel"),
+        ((256, 256, 256, 1024, (s256,) * 3), pkg.FLOW_STAGED, pkg.TILE_128x128,
+         "bgemm_big_kernel"),
+        ((256, 256, 256, 1024, (s256,) * 3), pkg.FLOW_DIRECT, pkg.TILE_128x128,
+         "bgemm_big_kernel"),
+        ((300, 260, 96, 1024, (300 * 96, 96 * 260, 300 * 260)), pkg.FLOW_REG, pkg.TILE_128x128,
+         "bgemm_reg_kernel"),
+        ((300, 260, 96, 1024, (300 * 96, 96 * 260, 300 * 260)), pkg.FLOW_STAGED,
+         pkg.TILE_128x128, "bgemm_emu_kernel"),
+        ((64, 64, 64, 16, (4096,) * 3), pkg.FLOW_REG, pkg.TILE_64x64, "bgemm_reg_kernel"),
+        ((64, 64, 64, 16, (4096,) * 3), pkg.FLOW_STAGED, pkg.TILE_64x64, "bgemm_emu_kernel"),
+        # B rows without 16-byte vectors (n odd): REG falls back to 64x64
+        ((1100, 1101, 512, 1, (0, 0, 0)), pkg.FLOW_REG, pkg.TILE_64x64, "bgemm_reg_kernel"),
+    ]
+    for (m, n, k, batch, st), flow, tile, kernel in auto_cases:
+        assert _resolve(m, n, k, batch, st, policy=pkg.Policy(flow, 1, pkg.TILE_AUTO),
+                        **apart) == (0, (flow, 1, tile)), (m, n, k, flow)
+        assert _resolve.kernel == kernel, (m, n, k, flow, _resolve.kernel)
     lib = pkg.load()
     assert lib.sgemm_emu_resolve_policy(4, 4, 4, ctypes.c_void_p(PA), 4, ctypes.c_void_p(PB), 4,
                                         ctypes.c_void_p(PC), 4, 1, S(0, 0, 0), None,
@@ -409,11 +431,14 @@ def test_scan_validation():
 def test_split_validation():
     lib = pkg.load()
     P = ctypes.c_void_p
-    assert lib.sgemm_emu_split(-1, P(PA), P(PB), P(PC), P(0)) == -1
-    assert lib.sgemm_emu_split(0, P(0), P(0), P(0), P(0)) == 0
-    assert lib.sgemm_emu_split(16, P(0), P(PB), P(PC), P(0)) == -3
-    assert lib.sgemm_emu_split(16, P(PA), P(PA + 8), P(PC), P(0)) == -5
-    assert lib.sgemm_emu_split(1 << 62, P(PA), P(PB), P(PC), P(0)) == -1
+    for form in (pkg.SPLIT_SCALAR, pkg.SPLIT_PAIR, pkg.SPLIT_EIGHT):
+        assert lib.sgemm_emu_split(-1, P(PA), P(PB), P(PC), form, P(0)) == -1
+        assert lib.sgemm_emu_split(0, P(0), P(0), P(0), form, P(0)) == 0
+        assert lib.sgemm_emu_split(16, P(0), P(PB), P(PC), form, P(0)) == -3
+        assert lib.sgemm_emu_split(16, P(PA), P(PA + 8), P(PC), form, P(0)) == -5
+        assert lib.sgemm_emu_split(1 << 62, P(PA), P(PB), P(PC), form, P(0)) == -1
+    assert lib.sgemm_emu_split(16, P(PA), P(PB), P(PC), 3, P(0)) == -8
+    assert lib.sgemm_emu_split(16, P(PA), P(PB), P(PC), -1, P(0)) == -8
 
 
 def test_strerror_covers_codes():
