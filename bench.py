@@ -8,7 +8,9 @@ A step is one sgemm_emu_batched call over the whole batch of the workload
 (every step of the path: operand loads, split, three MFMA products, combine
 and store), with inputs already resident in HBM, under the policy the
 library picks for it (or the one given).  The default workload is the
-batched one, 4096 products of 128 x 128 x 128 (uniform(-1, 1) FP32, seed 2).
+largest configuration, one 8192 x 8192 x 8192 product (uniform(-1, 1) FP32,
+seed 4): the one bound by the matrix units, where the emulation's rate is
+measured against one third of the fp16 MFMA peak.
 
 The roofline's "traffic" is the HBM traffic a counter run measured for this
 workload and kernel (profiles/traffic.json), reported only while the
@@ -131,7 +133,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="gemm_128", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="gemm_8192", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--flow", type=int, default=pkg.FLOW_AUTO)
     ap.add_argument("--ec", type=int, default=1)
     ap.add_argument("--tile", type=int, default=pkg.TILE_AUTO)

@@ -22,8 +22,8 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import (assert_periodic, device, gate, gate_applies, gate_repeated, periodic_batch,
-                      to_np)
+from gpu_util import (assert_all_finite, assert_periodic, device, gate, gate_applies,
+                      gate_repeated, nan_output, periodic_batch, spread_items, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -207,4 +207,23 @@ def test_random_shapes_all_layouts(shape):
         s, oa, ob, lay = combo
         D = _run(A, B, C, oa, ob, lay, SHAPES[s])
         gate(D, ref, max(k, 1), f"acc random {shape} {_cid(combo)}",
-             max_gate=gate_applies(k, batch * m * n))
+             max_gate=gate_applies(ref))
+
+
+def test_workload_gemm_acc_128_sampled():
+    """The full workload (4096 items of D = A^T B + C, 128^3) in the launch
+    configuration the benchmark times: every output written (NaN
+    beforehand, finite after) and 64 whole items spread over the batch held
+    to the bar."""
+    w = synth.WORKLOADS["gemm_acc_128"]
+    print(f"case workload=gemm_acc_128 batch={w.batch}", flush=True)
+    At, B, C = synth.workload_inputs(w)
+    dev = device()
+    D = nan_output((w.batch, w.m, w.n))
+    pkg.sgemm_emu_batched_acc(At.to(dev), B.to(dev), C.to(dev), D, op_a=pkg.OP_T)
+    assert_all_finite(D, "gemm_acc_128")
+    items = spread_items(w.batch, 64)
+    ref = oracle.gemm_acc(At[items].numpy(), B[items].numpy(), C[items].numpy(), "T", "N")
+    got = to_np(D[torch.from_numpy(items).to(dev)])
+    e = gate(got, ref, w.k, "gemm_acc_128")
+    print(f"gemm_acc_128: err {e[0]:.3e} fp32 {e[1]:.3e}")

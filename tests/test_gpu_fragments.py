@@ -143,11 +143,20 @@ def _structured_f32():
     return np.concatenate([x, sub.view(np.float32), np.float32([65504, -65504, 0, -0.0])])
 
 
-def test_device_split_bit_exact():
+@pytest.mark.parametrize("form", [pkg.SPLIT_SCALAR, pkg.SPLIT_PAIR, pkg.SPLIT_EIGHT],
+                         ids=["scalar", "pair", "eight"])
+def test_device_split_bit_exact(form):
+    """Every device form of the split (one value, a packed pair, a vector of
+    eight: the forms the kernels use) against the oracle's split, bit for
+    bit, over a structured sweep of FP32 (every exponent of the domain and
+    sign, the low 13 bits exhaustively, every subnormal-hi value range)."""
     x = _structured_f32()
+    # 1 extra value: the last group of 8 is cut short (split one at a time)
+    x = np.concatenate([x, np.float32([1 + 2.0 ** -11])])
     hi_ref, lo_ref = oracle.split(x)
     xd = torch.from_numpy(x).to(device())
-    hi, lo = pkg.sgemm_emu_split(xd)
+    print(f"case split form={form} count={x.size}", flush=True)
+    hi, lo = pkg.sgemm_emu_split(xd, form=form)
     hi = to_np(hi).view(np.uint16)
     lo = to_np(lo).view(np.uint16)
     bad_hi = np.count_nonzero(hi != hi_ref)

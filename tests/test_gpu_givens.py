@@ -28,7 +28,7 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import device, gate, to_np
+from gpu_util import assert_all_finite, device, gate, nan_output, spread_items, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -115,15 +115,23 @@ def test_padded_leading_dimensions_and_strided_angles():
 
 @pytest.mark.parametrize("mode", list(MODES))
 def test_workload_givens_sampled(mode):
+    """The full workload: every output written (NaN beforehand, finite
+    after) and 512 whole items spread over the batch held to the bar."""
     w = synth.WORKLOADS["givens_64"]
     i, j = w.plane
     print(f"case workload=givens_64 mode={mode} batch={w.batch}", flush=True)
     c, s, B = synth.workload_inputs(w)
-    C = _run(i, j, c, s, B, mode=MODES[mode])
-    items = [0, 1, 4095, 131072, w.batch - 1]
+    C = nan_output((w.batch, w.m, w.n))
+    pkg.givens_emu_batched(i, j, c.to(device()), s.to(device()), B.to(device()), C,
+                           mode=MODES[mode])
+    assert_all_finite(C, f"givens_64 {mode}")
+    items = spread_items(w.batch, 512)
     ref = oracle.givens(i, j, c.numpy(), s.numpy(), B.numpy(), items=items)
-    e = gate(C[items], ref, K_EFF, f"givens_64 {mode}", max_gate=False)
+    got = to_np(C[torch.from_numpy(items).to(C.device)])
+    e = gate(got, ref, K_EFF, f"givens_64 {mode}", max_gate=False)
     print(f"givens_64 {mode}: err {e[0]:.3e} fp32 {e[1]:.3e}")
+    del C
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("mode", list(MODES))

@@ -20,7 +20,8 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
+from gpu_util import (assert_all_finite, assert_periodic, device, gate, gate_repeated, nan_output,
+                      periodic_batch, spread_items, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -78,15 +79,24 @@ def test_padded_leading_dimensions():
     assert np.all(out[:, :, 70:] == 9.0)
 
 
-def test_workload_householder_sampled():
+@pytest.mark.parametrize("mode", [pkg.HOUSEHOLDER_RULE, pkg.HOUSEHOLDER_LDS], ids=["rule", "lds"])
+def test_workload_householder_sampled(mode):
+    """The full workload in the launch configuration the benchmark times:
+    every output written (NaN beforehand, finite after) and 512 whole items
+    spread over the batch (2M outputs) held to the parity bar."""
     w = synth.WORKLOADS["householder_64"]
-    print(f"case workload=householder_64 batch={w.batch}", flush=True)
+    print(f"case workload=householder_64 mode={mode} batch={w.batch}", flush=True)
     u, B = synth.workload_inputs(w)
-    C = _run(u, B)
-    items = [0, 1, 4095, 131072, w.batch - 1]
+    C = nan_output((w.batch, w.m, w.n))
+    pkg.householder_emu_batched(u.to(device()), B.to(device()), C, mode=mode)
+    assert_all_finite(C, "householder_64")
+    items = spread_items(w.batch, 512)
     ref = oracle.householder(u.numpy(), B.numpy(), items=items)
-    e = gate(C[items], ref, 64, "householder_64")
-    print(f"householder_64: err {e[0]:.3e} fp32 {e[1]:.3e}")
+    got = to_np(C[torch.from_numpy(items).to(C.device)])
+    e = gate(got, ref, 64, f"householder_64 mode {mode}")
+    print(f"householder_64 mode {mode}: err {e[0]:.3e} fp32 {e[1]:.3e}")
+    del C
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("ncols", [64, 33, 130])

@@ -28,7 +28,8 @@ import torch
 import oracle
 import paper_2308_15152_amd as pkg
 import synth
-from gpu_util import assert_periodic, device, gate, gate_repeated, periodic_batch, to_np
+from gpu_util import (assert_all_finite, assert_periodic, device, gate, gate_repeated, nan_output,
+                      periodic_batch, spread_items, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -99,12 +100,16 @@ def test_unaligned_output_only():
 
 
 def test_workload_scan_sampled():
+    """The full workload: every output written (NaN beforehand, finite
+    after) and 4096 whole rows spread over the batch held to the bar."""
     w = synth.WORKLOADS["scan_2048"]
     print(f"case workload=scan_2048 rows={w.batch} len={w.n}", flush=True)
     (X,) = synth.workload_inputs(w)
-    Y = pkg.sgemm_emu_scan(X.to(device()))
-    rows = [0, 1, 31, 32, 4095, 65536, w.batch - 1]
-    Ys = to_np(Y[rows])
+    Y = nan_output((w.batch, w.n))
+    pkg.sgemm_emu_scan(X.to(device()), Y)
+    assert_all_finite(Y, "scan_2048")
+    rows = spread_items(w.batch, 4096)
+    Ys = to_np(Y[torch.from_numpy(rows).to(Y.device)])
     ref = oracle.scan(X[rows].numpy())
     e = gate(Ys, ref, _k_eff(w.n), "scan_2048", max_gate=False)
     print(f"scan_2048: err {e[0]:.3e} fp32 running sum {e[1]:.3e}")
