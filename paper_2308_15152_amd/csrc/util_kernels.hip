@@ -11,7 +11,9 @@ namespace sgemm_emu {
 
 // Each thread splits one group of 8 consecutive values with the chosen
 // device function; a group cut short by the end of x is split one value at
-// a time.
+// a time.  An element of a vector is copied to a scalar before its bits are
+// taken: this clang reads element 0 when __builtin_bit_cast is applied to
+// an indexed vector element directly.
 template <int FORM>
 __global__ __launch_bounds__(256) void split_kernel(int64_t count, const float* __restrict__ x,
                                                     uint16_t* __restrict__ hi,
@@ -29,18 +31,20 @@ __global__ __launch_bounds__(256) void split_kernel(int64_t count, const float* 
                 mfmae::tcec::split8(v, h, l);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    hi[i0 + e] = __builtin_bit_cast(uint16_t, h[e]);
-                    lo[i0 + e] = __builtin_bit_cast(uint16_t, l[e]);
+                    const _Float16 he = h[e], le = l[e];
+                    hi[i0 + e] = __builtin_bit_cast(uint16_t, he);
+                    lo[i0 + e] = __builtin_bit_cast(uint16_t, le);
                 }
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; e += 2) {
                     mfmae::tcec::half2_t h, l;
                     mfmae::tcec::split_pair(v[e], v[e + 1], h, l);
-                    hi[i0 + e] = __builtin_bit_cast(uint16_t, h[0]);
-                    hi[i0 + e + 1] = __builtin_bit_cast(uint16_t, h[1]);
-                    lo[i0 + e] = __builtin_bit_cast(uint16_t, l[0]);
-                    lo[i0 + e + 1] = __builtin_bit_cast(uint16_t, l[1]);
+                    const _Float16 h0 = h[0], h1 = h[1], l0 = l[0], l1 = l[1];
+                    hi[i0 + e] = __builtin_bit_cast(uint16_t, h0);
+                    hi[i0 + e + 1] = __builtin_bit_cast(uint16_t, h1);
+                    lo[i0 + e] = __builtin_bit_cast(uint16_t, l0);
+                    lo[i0 + e + 1] = __builtin_bit_cast(uint16_t, l1);
                 }
             }
             continue;
