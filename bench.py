@@ -23,7 +23,9 @@ FP32 product timed on the host cores for a bounded sample of the same
 workload; the accuracy of the GPU result on that sample is reported with it.
 
 ``--copy-calibration`` instead runs a plain device copy of known size, used
-to scale the HBM traffic counters of a profiler run.
+to scale the HBM traffic counters of a profiler run; ``--hbm-probe`` times the
+batched workloads' memory traffic without their arithmetic, the reference
+their HBM fraction is read against.
 """
 from __future__ import annotations
 
@@ -155,6 +157,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target host time of the CPU-baseline sample")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--hbm-probe", action="store_true",
+                    help="time the read-A, read-B, write-C traffic of the batched square "
+                         "workloads without their arithmetic (sgemm_emu_stream_probe) at 256, 512 "
+                         "and 1024 threads per item; one line per case")
     ap.add_argument("--paper-sweep", action="store_true",
                     help="time the batched experiment of Sec. 4.4.2 (256 products of "
                          "1024 x k . k x 1024) for every k of the sweep; one line per k")
@@ -176,6 +182,42 @@ def copy_calibration(steps: int):
     dt = (time.perf_counter() - t0) / steps
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "steps": steps,
                       "ms_per_copy": dt * 1e3, "GBps": 8 * n / dt / 1e9}), flush=True)
+
+
+def hbm_probe(steps: int, warmup: int):
+    """The HBM rate the batched products' access pattern reaches without
+    arithmetic: items of A, B, C with the workload's item sizes, one
+    workgroup per item reading A and B and writing C (nontemporal), timed
+    with HIP events on the stream the probe runs on."""
+    for name in ("gemm_128", "gemm_256e"):
+        w = synth.WORKLOADS[name]
+        assert w.m == w.n == w.k
+        A = torch.rand((w.batch, w.m, w.k), device="cuda")
+        B = torch.rand((w.batch, w.k, w.n), device="cuda")
+        C = torch.empty((w.batch, w.m, w.n), device="cuda")
+        nbytes = 3 * A.numel() * 4
+        for threads in (256, 512, 1024):
+            for _ in range(warmup):
+                pkg.sgemm_emu_stream_probe(A, B, C, threads=threads)
+            stream = torch.cuda.current_stream()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(steps):
+                pkg.sgemm_emu_stream_probe(A, B, C, threads=threads)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            ok = bool(torch.equal(C[-1], A[-1] + B[-1]))
+            print(json.dumps({"probe": "read A, read B, write C", "items_like": name,
+                              "items": w.batch, "item_bytes": A[0].numel() * 4,
+                              "threads_per_item": threads, "bytes": nbytes, "steps": steps,
+                              "us_per_launch": ms * 1e3, "GBps": nbytes / (ms * 1e-3) / 1e9,
+                              "frac_of_8TBps": nbytes / (ms * 1e-3) / 8e12, "checked": ok}),
+                  flush=True)
+        del A, B, C
+        torch.cuda.empty_cache()
 
 
 def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO, hh_mode=pkg.HOUSEHOLDER_RULE):
@@ -354,6 +396,9 @@ def main():
     pkg.load()
     if args.copy_calibration:
         copy_calibration(args.steps)
+        return
+    if args.hbm_probe:
+        hbm_probe(args.steps, args.warmup)
         return
 
     if args.paper_sweep:

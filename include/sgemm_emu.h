@@ -429,6 +429,21 @@ int mfmae_foreach(int shape, int use, int lane, int* i_out, int* j_out);
 int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
                     hipStream_t stream);
 
+/* ---- Measurement reference ------------------------------------------------
+ * The memory traffic of a batched product without its arithmetic: for
+ * t < items, C_t := A_t + B_t elementwise over item_elems floats, one
+ * workgroup of `threads` threads per item (256, 512 or 1024), 16-byte loads
+ * of A and B and nontemporal 16-byte stores of C.  With the item sizes of a
+ * batched workload (A, B, C of m k, k n, m n floats) it moves the same bytes
+ * as the product in the same per-item pattern, so its rate is the HBM rate
+ * that access pattern reaches on the device.  A, B, C are device pointers
+ * to items * item_elems floats each, 16-byte aligned, C not overlapping A
+ * or B; item_elems is a positive multiple of 4 below 2^31.
+ * Errors: _DIM, _NULL, _UNSUPPORTED (threads, alignment or item_elems),
+ * _ALIAS, _HIP. */
+int sgemm_emu_stream_probe(int64_t items, int64_t item_elems, const float* A, const float* B,
+                           float* C, int threads, hipStream_t stream);
+
 /* ---- Diagnostics ------------------------------------------------------- */
 /* Static text for a status code. */
 const char* sgemm_emu_strerror(int code);

@@ -24,7 +24,7 @@ __all__ = [
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
-    "sgemm_emu_xcd_order", "sgemm_emu_tile_order",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
     "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS", "SPLIT_SCALAR", "SPLIT_PAIR", "SPLIT_EIGHT",
     "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
@@ -54,7 +54,7 @@ EXPORTED_SYMBOLS = (
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
-    "sgemm_emu_xcd_order", "sgemm_emu_tile_order",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
 )
 
 
@@ -129,6 +129,7 @@ def load():
         "sgemm_emu_last_hip_error": ([], i32),
         "sgemm_emu_xcd_order": ([i32, P], i32),
         "sgemm_emu_tile_order": ([i32, i32, P, P], i32),
+        "sgemm_emu_stream_probe": ([i64, i64, P, P, P, i32, P], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -305,6 +306,27 @@ def sgemm_emu_tile_order(tiles_m: int, tiles_n: int):
                                        cols.ctypes.data_as(ctypes.c_void_p)),
            "sgemm_emu_tile_order")
     return rows, cols
+
+
+def sgemm_emu_stream_probe(A, B, C, *, threads: int = 256, stream=None):
+    """Measurement reference: C[t] := A[t] + B[t] for every item t of
+    [items, ...] contiguous float32 device tensors of one shape, one
+    workgroup of ``threads`` threads per item (the read-A, read-B, write-C
+    traffic of a batched product without its arithmetic)."""
+    import torch
+
+    for name, t in (("A", A), ("B", B), ("C", C)):
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 device tensor")
+    if A.shape != B.shape or A.shape != C.shape or A.dim() < 1:
+        raise ValueError("A, B and C must have one shape [items, ...]")
+    items = A.shape[0]
+    per = A.numel() // max(items, 1)
+    with _on_device(A, B, C):
+        rc = load().sgemm_emu_stream_probe(items, per, _ptr(A), _ptr(B), _ptr(C), int(threads),
+                                           _stream(stream))
+    _check(rc, "sgemm_emu_stream_probe")
+    return C
 
 
 def sgemm_emu_batched_ex(A, B, C=None, *, policy: Policy, stream=None):

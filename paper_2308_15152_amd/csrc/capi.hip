@@ -661,6 +661,25 @@ int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
+int sgemm_emu_stream_probe(int64_t items, int64_t item_elems, const float* A, const float* B,
+                           float* C, int threads, hipStream_t stream) {
+    if (items < 0 || item_elems < 0) return SGEMM_EMU_ERR_DIM;
+    if (items == 0) return SGEMM_EMU_OK;
+    if (A == nullptr || B == nullptr || C == nullptr) return SGEMM_EMU_ERR_NULL;
+    if (threads != 256 && threads != 512 && threads != 1024) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (item_elems == 0 || item_elems % 4 != 0 || item_elems >= (int64_t(1) << 31))
+        return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (!aligned16(A) || !aligned16(B) || !aligned16(C)) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if (items > INT64_MAX / item_elems) return SGEMM_EMU_ERR_DIM;
+    const Extent ea = extent(A, items, 1, item_elems, item_elems, item_elems);
+    const Extent eb = extent(B, items, 1, item_elems, item_elems, item_elems);
+    const Extent ec = extent(C, items, 1, item_elems, item_elems, item_elems);
+    if (!all_ok({ea, eb, ec})) return SGEMM_EMU_ERR_DIM;
+    if (overlap(ec, ea) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
+    hipError_t e = sgemm_emu::launch_stream_probe(items, item_elems, A, B, C, threads, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
 const char* sgemm_emu_strerror(int code) {
     switch (code) {
         case SGEMM_EMU_OK: return "success";

@@ -109,6 +109,10 @@ hipError_t launch_scan(const ScanArgs& a, hipStream_t stream);
 hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* lo, int form,
                         hipStream_t stream);
 
+// C_t = A_t + B_t over items of n floats, one workgroup of `threads` per item.
+hipError_t launch_stream_probe(int64_t items, int64_t n, const float* A, const float* B, float* C,
+                               int threads, hipStream_t stream);
+
 hipError_t launch_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
                             hipStream_t stream);
 

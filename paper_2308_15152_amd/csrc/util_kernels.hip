@@ -75,6 +75,46 @@ hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* l
     return hipGetLastError();
 }
 
+// Measurement reference: the read-A, read-B, write-C traffic of a batched
+// product without its arithmetic.  One workgroup per item (item =
+// blockIdx.x + item0), 16-byte loads, nontemporal 16-byte stores (as the
+// full-tile kernel stores C).
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <int NT>
+__global__ __launch_bounds__(NT) void stream_probe_kernel(int64_t item0, int64_t n4,
+                                                          const f32x4_t* __restrict__ A,
+                                                          const f32x4_t* __restrict__ B,
+                                                          f32x4_t* __restrict__ C) {
+    const int64_t base = (item0 + blockIdx.x) * n4;
+    for (int64_t i = threadIdx.x; i < n4; i += NT) {
+        const f32x4_t v = A[base + i] + B[base + i];
+        __builtin_nontemporal_store(v, &C[base + i]);
+    }
+}
+
+hipError_t launch_stream_probe(int64_t items, int64_t n, const float* A, const float* B, float* C,
+                               int threads, hipStream_t stream) {
+    const int64_t n4 = n / 4;
+    const auto* a = reinterpret_cast<const f32x4_t*>(A);
+    const auto* b = reinterpret_cast<const f32x4_t*>(B);
+    auto* c = reinterpret_cast<f32x4_t*>(C);
+    const int64_t per_launch = (int64_t(1) << 31) / threads - 1;
+    for (int64_t i0 = 0; i0 < items; i0 += per_launch) {
+        const unsigned g = (unsigned)(items - i0 < per_launch ? items - i0 : per_launch);
+        if (threads == 256)
+            hipLaunchKernelGGL(stream_probe_kernel<256>, dim3(g), dim3(256), 0, stream, i0, n4, a, b, c);
+        else if (threads == 512)
+            hipLaunchKernelGGL(stream_probe_kernel<512>, dim3(g), dim3(512), 0, stream, i0, n4, a, b, c);
+        else
+            hipLaunchKernelGGL(stream_probe_kernel<1024>, dim3(g), dim3(1024), 0, stream, i0, n4, a, b,
+                               c);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <class S>
 __global__ __launch_bounds__(64) void mma_probe_kernel(const uint16_t* __restrict__ a,
                                                        const uint16_t* __restrict__ b,

@@ -528,3 +528,23 @@ def test_header_constants_match_binding():
     assert codes == list(range(-8, 0))
     for code in codes:
         assert "unknown" not in pkg.sgemm_emu_strerror(code)
+
+
+def test_stream_probe_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    n = 1 << 14
+    far = [P(1 << 40), P(2 << 40), P(3 << 40)]
+    assert lib.sgemm_emu_stream_probe(-1, n, *far, 256, P(0)) == -1
+    assert lib.sgemm_emu_stream_probe(4, -4, *far, 256, P(0)) == -1
+    assert lib.sgemm_emu_stream_probe(0, n, P(0), P(0), P(0), 256, P(0)) == 0
+    assert lib.sgemm_emu_stream_probe(4, n, P(0), far[1], far[2], 256, P(0)) == -3
+    for threads in (0, 128, 2048):
+        assert lib.sgemm_emu_stream_probe(4, n, *far, threads, P(0)) == -6
+    assert lib.sgemm_emu_stream_probe(4, 6, *far, 256, P(0)) == -6          # not whole vectors
+    assert lib.sgemm_emu_stream_probe(4, 1 << 31, *far, 256, P(0)) == -6    # item too long
+    assert lib.sgemm_emu_stream_probe(4, n, P((1 << 40) + 4), far[1], far[2], 256, P(0)) == -6
+    assert lib.sgemm_emu_stream_probe(1 << 40, 1 << 30, *far, 256, P(0)) == -1  # span wraps
+    # C overlapping A
+    assert lib.sgemm_emu_stream_probe(4, n, far[0], far[1], P((1 << 40) + 4 * n), 256,
+                                      P(0)) == -5

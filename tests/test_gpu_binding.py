@@ -103,3 +103,15 @@ def test_calls_from_several_threads():
         for r in range(10):
             got = to_np(results[i][r])
             assert np.array_equal(got.view(np.uint32), alone[i].view(np.uint32)), (i, r)
+
+
+@pytest.mark.parametrize("threads", [256, 512, 1024])
+def test_stream_probe_computes_the_sum(threads):
+    """The measurement reference moves A, B and C and adds: C = A + B exactly."""
+    dev = device()
+    g = torch.Generator().manual_seed(threads)
+    A = torch.rand((37, 64, 68), generator=g).to(dev)
+    B = torch.rand((37, 64, 68), generator=g).to(dev)
+    C = torch.full_like(A, float("nan"))
+    pkg.sgemm_emu_stream_probe(A, B, C, threads=threads)
+    assert torch.equal(C, A + B)
