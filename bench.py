@@ -157,6 +157,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target host time of the CPU-baseline sample")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--fp16-reference", action="store_true",
+                    help="time the vendor library's plain fp16 and bf16 GEMM (torch.mm) on the "
+                         "workload's shape: the matrix-unit rate a tuned GEMM reaches on this "
+                         "device and clock, context for the emulation's three products (one line "
+                         "per dtype; not the benchmark's value)")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="time the read-A, read-B, write-C traffic of the batched square "
                          "workloads without their arithmetic (sgemm_emu_stream_probe) at 256, 512 "
@@ -216,6 +221,45 @@ def hbm_probe(steps: int, warmup: int):
                               "us_per_launch": ms * 1e3, "GBps": nbytes / (ms * 1e-3) / 1e9,
                               "frac_of_8TBps": nbytes / (ms * 1e-3) / 8e12, "checked": ok}),
                   flush=True)
+        del A, B, C
+        torch.cuda.empty_cache()
+
+
+def fp16_reference(name: str, steps: int, warmup: int):
+    """The vendor library's plain half-precision GEMM on the workload's
+    shape (one product of each item, as a batched matmul), timed with HIP
+    events: how fast a tuned single fp16 product runs here.  The emulation
+    issues three such products, so a third of this rate is what it would
+    reach at the same matrix-unit efficiency."""
+    w = synth.WORKLOADS[name]
+    assert w.kind == "gemm"
+    for dt, label in ((torch.float16, "fp16"), (torch.bfloat16, "bf16")):
+        A = torch.rand((w.batch, w.m, w.k), device="cuda", dtype=dt)
+        B = torch.rand((w.batch, w.k, w.n), device="cuda", dtype=dt)
+        C = torch.empty((w.batch, w.m, w.n), device="cuda", dtype=dt)
+
+        def call():
+            if w.batch == 1:
+                torch.mm(A[0], B[0], out=C[0])
+            else:
+                torch.bmm(A, B, out=C)
+        for _ in range(warmup):
+            call()
+        stream = torch.cuda.current_stream()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        tf = w.flops / (ms * 1e-3) / 1e12
+        print(json.dumps({"reference": f"torch {'mm' if w.batch == 1 else 'bmm'} {label}",
+                          "workload": name, "steps": steps, "ms_per_step": ms, "TFLOPs": tf,
+                          "frac_of_dense_peak": tf / PEAK_FP16_MFMA_TFLOPS,
+                          "emulation_at_same_efficiency_TFLOPs": tf / 3}), flush=True)
         del A, B, C
         torch.cuda.empty_cache()
 
@@ -399,6 +443,9 @@ def main():
         return
     if args.hbm_probe:
         hbm_probe(args.steps, args.warmup)
+        return
+    if args.fp16_reference:
+        fp16_reference(args.workload, args.steps, args.warmup)
         return
 
     if args.paper_sweep:
