@@ -18,9 +18,11 @@ kernel's sources are unchanged since that run.
 
 One JSON line is printed with the emulated TFLOP/s, the roofline of the
 dominant kernel (its average duration from HIP events recorded on the stream
-the kernel is launched on) and, as a reported baseline, the oracle's plain
-FP32 product timed on the host cores for a bounded sample of the same
-workload; the accuracy of the GPU result on that sample is reported with it.
+the kernel is launched on), the median, minimum and maximum of single
+launches (from an event recorded after every call of the timed region) and,
+as a reported baseline, the oracle's plain FP32 product timed on the host
+cores for a bounded sample of the same workload; the accuracy of the GPU
+result on that sample is reported with it.
 
 ``--copy-calibration`` instead runs a plain device copy of known size, used
 to scale the HBM traffic counters of a profiler run; ``--hbm-probe`` times the
@@ -154,6 +156,10 @@ def parse():
                          "and time one replay of it: per-step time without the host's "
                          "launch overhead, for launch-bound workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-launch-spread", action="store_true",
+                    help="record no event between the timed calls (each adds about 2 us of host "
+                         "time per call, which shows only where the host's launch rate sets the "
+                         "step time); per_launch is then null")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="target host time of the CPU-baseline sample")
     ap.add_argument("--copy-calibration", action="store_true")
@@ -503,18 +509,34 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         call()  # one untimed replay
         torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # one event before the first call and one after every call (a marker on
+    # the stream, no work): the first and last bound the timed region, the
+    # ones between give the spread of single launches
+    spread = not (args.graph or args.no_launch_spread)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1 if spread else 2)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(launches):
-        call()
-    ev1.record(stream)
+    evs[0].record(stream)
+    if spread:
+        for i in range(launches):
+            call()
+            evs[i + 1].record(stream)
+    else:
+        for _ in range(launches):
+            call()
+        evs[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_events = ev0.elapsed_time(ev1)
+    ms_events = evs[0].elapsed_time(evs[-1])
     ms_step = ms_events / args.steps
+    per_launch = None
+    if spread:
+        d = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(launches))
+        h = len(d) // 2
+        median = d[h] if len(d) % 2 else 0.5 * (d[h - 1] + d[h])
+        per_launch = {"median_ms": median, "min_ms": d[0], "max_ms": d[-1],
+                      "value_at_median": (w.flops / (median * 1e-3)
+                                          / (1e9 if w.kind == "scan" else 1e12))}
 
     flops = w.flops
     tflops = flops / (ms_step * 1e-3) / 1e12
@@ -585,6 +607,7 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
         "frac_fp16_mfma_over_3": tflops / (PEAK_FP16_MFMA_TFLOPS / 3),
         "hbm_GBps_algorithmic": bytes_alg / (ms_step * 1e-3) / 1e9,
         "wall_s_timed": wall,
+        "per_launch": per_launch,
         "roofline": roof,
         "cpu_baseline": None,
     }
