@@ -182,9 +182,9 @@ int sgemm_emu_batched_ex(int m, int n, int k,
  * 128x256, and the direct and staged flows with tile 128x128, run a
  * pipelined full-tile kernel when m and n are multiples of the tile, k is a
  * positive multiple of 32, A and B rows are 16-byte aligned and a chunk's
- * byte offsets fit in 32 bits ((rows of the tile x lda + 32) x 4 < 2^32 and
- * (32 ldb + columns of the tile) x 4 < 2^32: lda below about 2^30 / tile
- * rows, ldb below about 2^25); otherwise the general LDS kernel (128x256
+ * byte offsets stay below 2^31 ((rows of the tile x lda + 32) x 4 < 2^31
+ * and (32 ldb + columns of the tile) x 4 < 2^31: lda below about 2^29 /
+ * tile rows, ldb below about 2^24); otherwise the general LDS kernel (128x256
  * has none: SGEMM_EMU_ERR_POLICY).  Without error correction (ec = 0, for
  * measuring what the correction costs), the split flow with tile 128x128
  * or 128x256 runs the same full-tile kernel under the same conditions, and

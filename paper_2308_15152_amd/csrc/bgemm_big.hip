@@ -201,7 +201,7 @@ __device__ inline void load_stage(Stage<CF>& st, const StageMap<CF>& sm, int k0)
             f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, sm.a_off[u] + 16, 0, 0));
     }
     const __amdgpu_buffer_rsrc_t rb = raw_rsrc(sm.b + (int64_t)k0 * sm.ldb);
-    const uint32_t row = (uint32_t)sm.ldb * 4u;  // bytes; a chunk fits in 32 bits (offsets_fit)
+    const uint32_t row = (uint32_t)sm.ldb * 4u;  // bytes; a chunk spans under 2^31 (offsets_fit)
     if constexpr (CF::FLOW == BIG_SPLIT) {
 #pragma unroll
         for (int r = 0; r < CF::B_QUADS; ++r)
@@ -219,10 +219,14 @@ __device__ inline void load_stage(Stage<CF>& st, const StageMap<CF>& sm, int k0)
     }
 }
 
-// The byte offsets of StageMap fit in 32 bits.
+// The byte offsets of StageMap and the row offsets of load_stage stay below
+// 2^31, so that no buffer offset depends on how the hardware treats the top
+// bit of a 32-bit offset.  Larger leading dimensions (128 rows of over 2^22
+// floats, 32 rows of over 2^24) take the general kernel, which addresses
+// with 64-bit pointers.
 template <class CF>
 bool offsets_fit(const GemmArgs& a) {
-    const int64_t lim = (int64_t)1 << 32;
+    const int64_t lim = (int64_t)1 << 31;
     return ((int64_t)CF::BM * a.lda + CF::BK) * 4 < lim &&
            ((int64_t)CF::BK * a.ldb + CF::BN) * 4 < lim;
 }

@@ -196,10 +196,10 @@ def test_resolve_policy():
     # k not a multiple of 4: no 16-byte A rows, so the LDS flow
     assert _resolve(128, 128, 130)[1][0] == pkg.FLOW_SPLIT
     assert _resolve.kernel == "bgemm_emu_kernel"
-    # full tiles whose chunk byte offsets would not fit in 32 bits: A rows
-    # 2^23 floats apart (128 rows x 2^25 bytes), B rows 2^25 floats apart
-    # (fake operands 1 TiB apart, so that the spans do not overlap)
-    big = 1 << 23
+    # full tiles whose chunk byte offsets would reach 2^31: A rows 2^22
+    # floats apart (128 rows x 2^24 bytes), B rows 2^24 floats apart (fake
+    # operands 1 TiB apart, so that the spans do not overlap)
+    big = 1 << 22
     pol = pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_128x128)
     lib = pkg.load()
     out = pkg.Policy()
@@ -214,8 +214,8 @@ def test_resolve_policy():
         return kern.value.decode()
 
     assert far(big, 256) == "bgemm_emu_kernel"
-    assert far(256, 1 << 25) == "bgemm_emu_kernel"
-    assert far(big - 256, (1 << 25) - 256) == "bgemm_big_kernel"
+    assert far(256, 1 << 24) == "bgemm_emu_kernel"
+    assert far(big - 256, (1 << 24) - 256) == "bgemm_big_kernel"
     # the paper's flows on full 128 x 128 tiles run in the full-tile kernel
     for flow in (pkg.FLOW_DIRECT, pkg.FLOW_STAGED):
         assert _resolve(8192, 8192, 8192, policy=pkg.Policy(flow, 1, pkg.TILE_128x128)) == (

@@ -6,7 +6,8 @@ the C ABI on the GPU.
   tiles and ragged tails, and every k-loop path of the register-direct
   flow;
 * edge cases: k = 0, empty problems, a single element, broadcast operands
-  (zero batch stride), padded leading dimensions, unaligned pointers (the
+  (zero batch stride), padded leading dimensions, leading dimensions at and
+  just past the full-tile kernel's offset limit, unaligned pointers (the
   scalar-load path);
 * exactness on integer inputs in binary16 range;
 * the error-correction-off control must be visibly worse (the correction
@@ -155,6 +156,60 @@ def test_full_tile_kernel_shapes(flow, tile, shape):
     pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=policy)
     ref = oracle.gemm(A.numpy(), B.numpy())
     gate(to_np(Cd), ref, k, f"full-tile {tile} {shape}")
+
+
+LIMIT_CASES = [(pkg.FLOW_SPLIT, pkg.TILE_128x128, 128, 128),
+               (pkg.FLOW_SPLIT, pkg.TILE_256x128, 256, 128),
+               (pkg.FLOW_SPLIT, pkg.TILE_128x256, 128, 256),
+               (pkg.FLOW_DIRECT, pkg.TILE_128x128, 128, 128),
+               (pkg.FLOW_STAGED, pkg.TILE_128x128, 128, 128)]
+
+
+@pytest.mark.parametrize("flow,tile,bm,bn", LIMIT_CASES,
+                         ids=["split-128x128", "split-256x128", "split-128x256", "direct-128x128",
+                              "staged-128x128"])
+def test_full_tile_kernel_at_its_offset_limit(flow, tile, bm, bn):
+    """The largest leading dimensions the full-tile kernel takes (a chunk's
+    byte offsets just below 2^31: A rows about 2^29 / bm floats apart, B rows
+    about 2^24; operands of 2-4 GB) and one step past that on A and on B,
+    where the general kernel takes over: all three agree with the oracle.
+    Two chunks, so that the chunk descriptors move along A and B too."""
+    dev = device()
+    m, n, k = bm, bn, 64
+
+    def lda_max(rows):  # largest multiple of 4 with (rows lda + 32) 4 < 2^31
+        return ((2**29 - 32 - 1) // rows) // 4 * 4
+
+    def ldb_max(cols):  # largest multiple of 4 with (32 ldb + cols) 4 < 2^31
+        return ((2**29 - cols - 1) // 32) // 4 * 4
+
+    A, B = synth.gemm_inputs(1, m, n, k, seed=71 + bm + bn + flow)
+    ref = oracle.gemm(A.numpy(), B.numpy())
+    policy = pkg.Policy(flow, 1, tile)
+    # the general kernel has no 128 x 256 tile: past the limit that case
+    # names 128 x 128, whose limit on ldb is higher
+    past_policy, past_bn = policy, bn
+    if tile == pkg.TILE_128x256:
+        past_policy, past_bn = pkg.Policy(flow, 1, pkg.TILE_128x128), 128
+    for lda, ldb, pol, full in [(lda_max(bm), ldb_max(bn), policy, True),
+                                (lda_max(bm) + 4, n, past_policy, False),
+                                (k, ldb_max(past_bn) + 4, past_policy, False)]:
+        print(f"case offset limit flow={flow} tile={tile} lda={lda} ldb={ldb}", flush=True)
+        Ab = torch.empty((1, m, lda), device=dev)
+        Bb = torch.empty((1, k, ldb), device=dev)
+        Ab[:, :, :k] = A.to(dev)
+        Bb[:, :, :n] = B.to(dev)
+        Ad, Bd = Ab[:, :, :k], Bb[:, :, :n]
+        Cd = nan_output((1, m, n))
+        _, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, Cd, policy=pol)
+        if full:
+            assert kern in ("bgemm_big_kernel", "bgemm_big_stream_kernel"), kern
+        else:
+            assert kern == "bgemm_emu_kernel", kern
+        pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=pol)
+        gate(to_np(Cd), ref, k, f"offset limit {tile} lda={lda} ldb={ldb}")
+        del Ab, Bb, Ad, Bd, Cd
+        torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("batch,k", [(600, 96), (513, 32), (300, 160)])
