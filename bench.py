@@ -381,14 +381,19 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
     per_item = w.flops / w.batch
     scale, unit = (1e9, "Gelem/s") if w.kind == "scan" else (1e12, "TFLOP/s")
     if w.batch == 1:
-        # one huge product: sample whole output rows instead of items
+        # one huge product: sample whole output rows instead of items,
+        # calibrated at full parallelism (at least one row per thread) and
+        # grown until the calibration takes an eighth of the target
         A, B = host_inputs
-        rows = 8
-        t0 = time.perf_counter()
-        oracle.gemm(A[0, :rows].numpy()[None], B[0].numpy()[None], want=("c32",))
-        dt = time.perf_counter() - t0
-        est = max(1, int(rows * target_s / max(dt, 1e-3)))
-        rows = min(w.m, est)
+        rows = min(w.m, threads)
+        while True:
+            t0 = time.perf_counter()
+            oracle.gemm(A[0, :rows].numpy()[None], B[0].numpy()[None], want=("c32",))
+            dt = time.perf_counter() - t0
+            if dt >= target_s / 8 or rows >= w.m:
+                break
+            rows = min(w.m, rows * 4)
+        rows = min(w.m, max(rows, int(rows * target_s / max(dt, 1e-6))))
         t0 = time.perf_counter()
         oracle.gemm(A[0, :rows].numpy()[None], B[0].numpy()[None], want=("c32",))
         dt = time.perf_counter() - t0
@@ -404,7 +409,7 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
                "sample": "256 random elements"}
         sample = f"{rows} of {w.m} output rows of the {w.m}x{w.n}x{w.k} product"
         return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
-                "kind": "oracle", "sample": sample, "seconds": dt}, acc
+                "kind": "oracle", "sample": sample, "seconds": dt, "host": host_cpu()}, acc
 
     # calibrate at full parallelism (at least one item per thread), growing
     # the sample until it takes an eighth of the target
@@ -436,7 +441,26 @@ def cpu_baseline(w, host_inputs, C_dev, target_s: float):
            "sample": f"items 0..{len(acc_items) - 1}"}
     sample = f"{n} of {w.batch} batch items" + (f", {reps} passes" if reps > 1 else "")
     return {"value": per_item * n * reps / dt / scale, "unit": unit, "cores": threads,
-            "kind": "oracle", "sample": sample, "seconds": dt}, acc
+            "kind": "oracle", "sample": sample, "seconds": dt, "host": host_cpu()}, acc
+
+
+def host_cpu():
+    """The host the CPU baseline ran on: CPU model, logical CPUs, and the CPUs
+    this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"model": model, "logical_cpus": os.cpu_count(), "usable_cpus": usable}
 
 
 def main():
