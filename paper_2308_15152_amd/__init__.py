@@ -88,6 +88,29 @@ _lib = None
 _NO_SWITCH = contextlib.nullcontext()
 
 
+class _CheckedInt32(ctypes.c_int32):
+    """int argument of the C ABI: a value outside the 32-bit range raises
+    instead of being wrapped (ctypes alone would pass 2^32 + 8 as 8)."""
+
+    @classmethod
+    def from_param(cls, value):
+        v = int(value)
+        if not -(1 << 31) <= v < (1 << 31):
+            raise ValueError(f"{v} does not fit the 32-bit int argument")
+        return ctypes.c_int32(v)
+
+
+class _CheckedInt64(ctypes.c_int64):
+    """int64_t argument of the C ABI, range-checked the same way."""
+
+    @classmethod
+    def from_param(cls, value):
+        v = int(value)
+        if not -(1 << 63) <= v < (1 << 63):
+            raise ValueError(f"{v} does not fit the 64-bit int argument")
+        return ctypes.c_int64(v)
+
+
 def lib_path() -> str:
     return os.environ.get("SGEMM_EMU_LIB", os.path.join(_HERE, LIB_NAME))
 
@@ -103,7 +126,7 @@ def load():
             f"{path} not found: build it first (python -c 'import __graft_entry__ as g; g.build()'"
             " or python paper_2308_15152_amd/build.py)")
     lib = ctypes.CDLL(path)
-    i32, i64, P = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+    i32, i64, P = _CheckedInt32, _CheckedInt64, ctypes.c_void_p
     ip = ctypes.POINTER(ctypes.c_int)
     sig = {
         "sgemm_emu_batched": ([i32, i32, i32, P, i32, P, i32, P, i32, i32, Stride, P], i32),
@@ -134,7 +157,7 @@ def load():
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
         fn.argtypes = args
-        fn.restype = res
+        fn.restype = ctypes.c_int if res is i32 else res  # plain int results
     _lib = lib
     return lib
 

@@ -441,6 +441,28 @@ def test_split_validation():
     assert lib.sgemm_emu_split(16, P(PA), P(PB), P(PC), -1, P(0)) == -8
 
 
+def test_binding_refuses_values_outside_the_argument_range():
+    """ctypes on its own wraps an int argument modulo 2^32 (a leading
+    dimension of 2^32 + 8 would reach the library as 8); the binding's
+    argument types refuse such values before any call."""
+    lib = pkg.load()
+    S = pkg.Stride
+    for bad in (1 << 31, (1 << 32) + 8, -(1 << 31) - 1):
+        with pytest.raises(ctypes.ArgumentError):
+            lib.sgemm_emu_batched(4, 4, 4, None, bad, None, 4, None, 4, 1, S(0, 0, 0), None)
+        with pytest.raises(ctypes.ArgumentError):
+            lib.mfmae_num_elements(bad, 0)
+    with pytest.raises(ctypes.ArgumentError):
+        lib.sgemm_emu_scan(1 << 63, 4, None, 4, None, 4, None)
+    # the edges of the range pass through to the library's own validation
+    assert lib.sgemm_emu_batched(4, 4, 4, None, (1 << 31) - 1, None, 4, None, 4, 1, S(0, 0, 0),
+                                 None) == -3
+    assert lib.sgemm_emu_batched(-(1 << 31), 4, 4, None, 4, None, 4, None, 4, 1, S(0, 0, 0),
+                                 None) == -1
+    assert lib.sgemm_emu_scan((1 << 63) - 1, 4, None, 4, None, 4, None) != 0
+    assert isinstance(lib.mfmae_num_elements(1, 0), int)
+
+
 def test_strerror_covers_codes():
     for code in range(-8, 1):
         assert "unknown" not in pkg.sgemm_emu_strerror(code)
