@@ -27,7 +27,9 @@ result on that sample is reported with it.
 ``--copy-calibration`` instead runs a plain device copy of known size, used
 to scale the HBM traffic counters of a profiler run; ``--hbm-probe`` times the
 batched workloads' memory traffic without their arithmetic, the reference
-their HBM fraction is read against.
+their HBM fraction is read against; ``--mfma-probe`` times the 8192^3
+product's arithmetic without its data movement, the reference its matrix-unit
+fraction is read against at the clock the device holds.
 """
 from __future__ import annotations
 
@@ -168,6 +170,10 @@ def parse():
                          "workload's shape: the matrix-unit rate a tuned GEMM reaches on this "
                          "device and clock, context for the emulation's three products (one line "
                          "per dtype; not the benchmark's value)")
+    ap.add_argument("--mfma-probe", action="store_true",
+                    help="time the full-tile kernel's products alone on the workload's shape "
+                         "(sgemm_emu_mfma_probe): the rate the matrix units reach for them at the "
+                         "clock the device holds; one line, not the benchmark's value")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="time the read-A, read-B, write-C traffic of the batched square "
                          "workloads without their arithmetic (sgemm_emu_stream_probe) at 256, 512 "
@@ -274,6 +280,46 @@ def fp16_reference(name: str, steps: int, warmup: int, dtypes=("fp16", "bf16"), 
         del A, B, C
         torch.cuda.empty_cache()
     return out
+
+
+def mfma_ceiling(name: str, steps: int, warmup: int, quiet=False):
+    """The full-tile kernel's three products alone on the workload's shape
+    (sgemm_emu_mfma_probe: same grid, waves and MFMA sequence on 128 x 256
+    tiles, operand fragments held in registers, no loads, split or LDS
+    traffic in the k loop), timed with HIP events: the rate the matrix units
+    reach for these products at the clock the device holds under them.
+    Returns the record."""
+    w = synth.WORKLOADS[name]
+    if w.kind != "gemm" or w.batch != 1 or w.m % 128 or w.n % 256 or w.k % 32:
+        raise SystemExit(f"--mfma-probe needs one product of full 128 x 256 tiles, not {name}")
+    g = torch.Generator(device="cuda").manual_seed(w.seed)
+    A = torch.rand((w.m, 32), device="cuda", generator=g) * 2 - 1
+    B = torch.rand((32, w.n), device="cuda", generator=g) * 2 - 1
+    C = torch.empty((w.m, w.n), device="cuda")
+
+    def call():
+        pkg.sgemm_emu_mfma_probe(A, B, w.k, C)
+    for _ in range(warmup):
+        call()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tf = w.flops / (ms * 1e-3) / 1e12
+    rec = {"reference": "the products alone (sgemm_emu_mfma_probe, kernel mfma_probe_kernel)",
+           "workload": name, "steps": steps, "ms_per_step": ms, "TFLOPs": tf,
+           "fp16_mfma_TFLOPs": 3 * tf, "frac_of_dense_peak": 3 * tf / PEAK_FP16_MFMA_TFLOPS}
+    if not quiet:
+        print(json.dumps(rec), flush=True)
+    del A, B, C
+    torch.cuda.empty_cache()
+    return rec
 
 
 def make_call(w, inputs, policy, givens_mode=pkg.GIVENS_AUTO, hh_mode=pkg.HOUSEHOLDER_RULE):
@@ -483,6 +529,9 @@ def main():
     if args.fp16_reference:
         fp16_reference(args.workload, args.steps, args.warmup)
         return
+    if args.mfma_probe:
+        mfma_ceiling(args.workload, args.steps, args.warmup)
+        return
 
     if args.paper_sweep:
         for k in synth.PAPER_SWEEP_K:
@@ -644,6 +693,13 @@ def bench_workload(args, name: str, cpu: bool) -> dict:
             "what": "torch.mm fp16 on the same shape, same device, after the timed region",
             "TFLOPs": ref["TFLOPs"], "frac_of_dense_peak": ref["frac_of_dense_peak"],
             "emulated_rate_over_a_third_of_it": tflops / (ref["TFLOPs"] / 3)}
+        # and the same products with their operands held in registers
+        cei = mfma_ceiling(w.name, 10, 3, quiet=True)
+        out["context_mfma_ceiling"] = {
+            "what": "the same three products alone (operands in registers, no loads, split or "
+                    "LDS traffic; sgemm_emu_mfma_probe), same device, after the timed region",
+            "TFLOPs": cei["TFLOPs"], "frac_of_dense_peak": cei["frac_of_dense_peak"],
+            "emulated_rate_over_it": tflops / cei["TFLOPs"]}
     if cpu:
         cb, acc = cpu_baseline(w, host_inputs, C, args.cpu_seconds)
         out["cpu_baseline"] = cb

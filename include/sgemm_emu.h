@@ -429,7 +429,7 @@ int mfmae_foreach(int shape, int use, int lane, int* i_out, int* j_out);
 int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
                     hipStream_t stream);
 
-/* ---- Measurement reference ------------------------------------------------
+/* ---- Measurement references -----------------------------------------------
  * The memory traffic of a batched product without its arithmetic: for
  * t < items, C_t := A_t + B_t elementwise over item_elems floats, one
  * workgroup of `threads` threads per item (256, 512 or 1024), 16-byte loads
@@ -443,6 +443,23 @@ int mfmae_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
  * _ALIAS, _HIP. */
 int sgemm_emu_stream_probe(int64_t items, int64_t item_elems, const float* A, const float* B,
                            float* C, int threads, hipStream_t stream);
+
+/* The arithmetic of the full-tile kernel without its data movement (the
+ * three products of Sec. 4.4 alone): on the m x n output, in 128 x 256 tiles
+ * with the same grid, task order, waves and MFMA sequence as the full-tile
+ * kernel, the operand fragments of the first k chunk (A[i][0..31],
+ * B[0..31][j]) are split once and held in registers, and the k loop runs
+ * the k / 32 chunks' products on them with no global loads, split or LDS
+ * traffic.  C := (k / 32) * (the emulated product of that chunk), written
+ * as the kernel writes C.  Its rate (2 m n k / time) is the rate the
+ * matrix units reach for these products at the clock the device holds
+ * under them.  m a multiple of 128, n of 256, k a positive multiple of 32;
+ * lda >= 32, ldb >= n, ldc >= n; A, B, C device pointers (only the first 32
+ * columns of A and the first 32 rows of B are read); C must not overlap
+ * them.  m = 0 or n = 0: no-op.
+ * Errors: _DIM, _UNSUPPORTED (sizes not multiples), _LD, _NULL, _ALIAS, _HIP. */
+int sgemm_emu_mfma_probe(int m, int n, int k, const float* A, int lda, const float* B, int ldb,
+                         float* C, int ldc, hipStream_t stream);
 
 /* ---- Diagnostics ------------------------------------------------------- */
 /* Static text for a status code. */

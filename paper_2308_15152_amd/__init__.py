@@ -25,6 +25,7 @@ __all__ = [
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
     "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
+    "sgemm_emu_mfma_probe",
     "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS", "SPLIT_SCALAR", "SPLIT_PAIR", "SPLIT_EIGHT",
     "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
@@ -55,6 +56,7 @@ EXPORTED_SYMBOLS = (
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
     "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
+    "sgemm_emu_mfma_probe",
 )
 
 
@@ -153,6 +155,7 @@ def load():
         "sgemm_emu_xcd_order": ([i32, P], i32),
         "sgemm_emu_tile_order": ([i32, i32, P, P], i32),
         "sgemm_emu_stream_probe": ([i64, i64, P, P, P, i32, P], i32),
+        "sgemm_emu_mfma_probe": ([i32, i32, i32, P, i32, P, i32, P, i32, P], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -349,6 +352,32 @@ def sgemm_emu_stream_probe(A, B, C, *, threads: int = 256, stream=None):
         rc = load().sgemm_emu_stream_probe(items, per, _ptr(A), _ptr(B), _ptr(C), int(threads),
                                            _stream(stream))
     _check(rc, "sgemm_emu_stream_probe")
+    return C
+
+
+def sgemm_emu_mfma_probe(A, B, k: int, C=None, *, stream=None):
+    """Measurement reference: the full-tile kernel's products for an m x n x k
+    product on 128 x 256 tiles, with the fragments of the first k chunk held
+    in registers (no loads, split or LDS traffic in the k loop).  A: [m, >= 32]
+    and B: [>= 32, n] float32 device tensors with contiguous rows (only
+    A[:, :32] and B[:32, :] are read); C: [m, n] (allocated if None) receives
+    (k / 32) * the emulated product A[:, :32] @ B[:32, :]."""
+    import torch
+
+    ba, m, ka, lda, _ = _matrix_view(A, "A")
+    bb, kb, n, ldb, _ = _matrix_view(B, "B")
+    if ba is not None or bb is not None:
+        raise ValueError("A and B must be 2-D")
+    if ka < 32 or kb < 32:
+        raise ValueError("A needs 32 columns and B 32 rows")
+    if C is None:
+        C = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    _check_shape(C, (m, n), "C")
+    _, _, _, ldc, _ = _matrix_view(C, "C")
+    with _on_device(A, B, C):
+        rc = load().sgemm_emu_mfma_probe(m, n, int(k), _ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc,
+                                         _stream(stream))
+    _check(rc, "sgemm_emu_mfma_probe")
     return C
 
 

@@ -680,6 +680,23 @@ int sgemm_emu_stream_probe(int64_t items, int64_t item_elems, const float* A, co
     return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
 }
 
+int sgemm_emu_mfma_probe(int m, int n, int k, const float* A, int lda, const float* B, int ldb,
+                         float* C, int ldc, hipStream_t stream) {
+    if (m < 0 || n < 0 || k < 0) return SGEMM_EMU_ERR_DIM;
+    if (m == 0 || n == 0) return SGEMM_EMU_OK;
+    if (k == 0 || m % 128 != 0 || n % 256 != 0 || k % 32 != 0) return SGEMM_EMU_ERR_UNSUPPORTED;
+    if ((int64_t)(m / 128) * (n / 256) > ((int64_t)1 << 31) / 512 - 1) return SGEMM_EMU_ERR_DIM;
+    if (lda < 32 || ldb < n || ldc < n) return SGEMM_EMU_ERR_LD;
+    if (A == nullptr || B == nullptr || C == nullptr) return SGEMM_EMU_ERR_NULL;
+    const Extent ea = extent(A, 1, m, 32, lda, 0);
+    const Extent eb = extent(B, 1, 32, n, ldb, 0);
+    const Extent ec = extent(C, 1, m, n, ldc, 0);
+    if (!all_ok({ea, eb, ec})) return SGEMM_EMU_ERR_DIM;
+    if (overlap(ec, ea) || overlap(ec, eb)) return SGEMM_EMU_ERR_ALIAS;
+    hipError_t e = sgemm_emu::launch_mfma_probe(m, n, k, A, lda, B, ldb, C, ldc, stream);
+    return e == hipSuccess ? SGEMM_EMU_OK : hip_fail(e);
+}
+
 const char* sgemm_emu_strerror(int code) {
     switch (code) {
         case SGEMM_EMU_OK: return "success";

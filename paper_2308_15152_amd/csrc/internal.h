@@ -113,6 +113,10 @@ hipError_t launch_split(int64_t count, const float* x, uint16_t* hi, uint16_t* l
 hipError_t launch_stream_probe(int64_t items, int64_t n, const float* A, const float* B, float* C,
                                int threads, hipStream_t stream);
 
+// m a multiple of 128, n of 256, k of 32 (k > 0); reads A[.][0..31], B[0..31][.].
+hipError_t launch_mfma_probe(int m, int n, int k, const float* A, int64_t lda, const float* B,
+                             int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
+
 hipError_t launch_mma_probe(int shape, const uint16_t* a, const uint16_t* b, float* d,
                             hipStream_t stream);
 

@@ -6,6 +6,7 @@
 #include "mfmae/frag.hpp"
 #include "mfmae/tcec.hpp"
 #include "sgemm_emu.h"
+#include "tiling.hpp"
 
 namespace sgemm_emu {
 
@@ -113,6 +114,114 @@ hipError_t launch_stream_probe(int64_t items, int64_t n, const float* A, const f
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// Measurement reference for the full-tile kernel's 128 x 256 tile: the same
+// grid, task numbering, waves (eight of 64 x 64, two per SIMD), MFMA
+// instruction (v_mfma_f32_32x32x16_f16), product order per k step (hi.hi for
+// the four blocks, then lo.hi, then hi.lo into the correction accumulator) and
+// epilogue, with the operand fragments of the tile's first k chunk built once
+// (split from A[.][0..31] and B[0..31][.]) and held in registers: the k loop
+// runs the products alone, without global loads, split or LDS traffic.  C
+// receives k / 32 times the emulated product of the first chunk,
+// A[.][0..31] B[0..31][.].
+struct MfmaProbeParams {
+    const float* A;
+    int64_t lda;
+    const float* B;
+    int64_t ldb;
+    float* C;
+    int64_t ldc;
+    int tiles_m, tiles_n;
+    int nk;  // k chunks of 32
+};
+
+__global__ __launch_bounds__(512, 2) void mfma_probe_kernel(MfmaProbeParams p) {
+    using mfmae::half8_t;
+    const TileRC rc = grouped_tile(xcd_task(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int l = threadIdx.x & 63;
+    const int g = l >> 5, j = l & 31;
+    const int r0 = rc.tm * 128 + (wave / 4) * 64;  // the wave's 64 x 64 sub-tile
+    const int c0 = rc.tn * 256 + (wave % 4) * 64;
+    // [k step][block]: lane (j, g) holds k = 16 s + 8 g + 0..7 of row / column j
+    half8_t ahi[2][2], alo[2][2], bhi[2][2], blo[2][2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            float x[8];
+            const float* ap = p.A + (int64_t)(r0 + 32 * t + j) * p.lda + 16 * s + 8 * g;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) x[v] = ap[v];
+            mfmae::tcec::split8(x, ahi[s][t], alo[s][t]);
+            const float* bp = p.B + (int64_t)(16 * s + 8 * g) * p.ldb + c0 + 32 * t + j;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) x[v] = bp[(int64_t)v * p.ldb];
+            mfmae::tcec::split8(x, bhi[s][t], blo[s][t]);
+        }
+    mfmae::f32x16_t acc[2][2], cor[2][2];
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                acc[tm][tn][e] = 0.0f;
+                cor[tm][tn][e] = 0.0f;
+            }
+    for (int c = 0; c < p.nk; ++c) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+#pragma unroll
+            for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+                for (int tn = 0; tn < 2; ++tn)
+                    acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[s][tm], bhi[s][tn],
+                                                                         acc[tm][tn], 0, 0, 0);
+#pragma unroll
+            for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+                for (int tn = 0; tn < 2; ++tn)
+                    cor[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(alo[s][tm], bhi[s][tn],
+                                                                         cor[tm][tn], 0, 0, 0);
+#pragma unroll
+            for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+                for (int tn = 0; tn < 2; ++tn)
+                    cor[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi[s][tm], blo[s][tn],
+                                                                         cor[tm][tn], 0, 0, 0);
+        }
+    }
+    // element e of a 32 x 32 block is row 8 (e / 4) + 4 g + e % 4, column j
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn) {
+            float* cp = p.C + (int64_t)(r0 + 32 * tm + 4 * g) * p.ldc + c0 + 32 * tn + j;
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                __builtin_nontemporal_store(
+                    __builtin_fmaf(cor[tm][tn][e], mfmae::tcec::kLoScaleInv, acc[tm][tn][e]),
+                    &cp[(int64_t)(8 * (e >> 2) + (e & 3)) * p.ldc]);
+        }
+}
+
+hipError_t launch_mfma_probe(int m, int n, int k, const float* A, int64_t lda, const float* B,
+                             int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
+    MfmaProbeParams p;
+    p.A = A;
+    p.lda = lda;
+    p.B = B;
+    p.ldb = ldb;
+    p.C = C;
+    p.ldc = ldc;
+    p.tiles_m = m / 128;
+    p.tiles_n = n / 256;
+    p.nk = k / 32;
+    hipLaunchKernelGGL(mfma_probe_kernel, dim3((unsigned)(p.tiles_m * p.tiles_n)), dim3(512), 0,
+                       stream, p);
+    return hipGetLastError();
 }
 
 template <class S>

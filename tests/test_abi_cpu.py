@@ -552,6 +552,24 @@ def test_header_constants_match_binding():
         assert "unknown" not in pkg.sgemm_emu_strerror(code)
 
 
+def test_mfma_probe_validation():
+    lib = pkg.load()
+    P = ctypes.c_void_p
+    a, b, c = P(1 << 40), P(2 << 40), P(3 << 40)
+
+    def mp(m=256, n=512, k=64, A=a, lda=64, B=b, ldb=512, C=c, ldc=512):
+        return lib.sgemm_emu_mfma_probe(m, n, k, A, lda, B, ldb, C, ldc, P(0))
+
+    assert mp(m=-128) == -1 and mp(k=-32) == -1
+    assert mp(m=0, A=P(0), B=P(0), C=P(0)) == 0 and mp(n=0) == 0
+    for bad in (dict(m=200), dict(n=384), dict(k=48), dict(k=0)):
+        assert mp(**bad) == -6, bad
+    assert mp(lda=31) == -2 and mp(ldb=511) == -2 and mp(ldc=500) == -2
+    assert mp(A=P(0)) == -3 and mp(C=P(0)) == -3
+    assert mp(C=P((1 << 40) + 1024)) == -5      # C over A's rows
+    assert mp(m=1 << 30, n=1 << 30) == -1       # more tiles than one launch counts
+
+
 def test_stream_probe_validation():
     lib = pkg.load()
     P = ctypes.c_void_p

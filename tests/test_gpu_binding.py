@@ -115,3 +115,33 @@ def test_stream_probe_computes_the_sum(threads):
     C = torch.full_like(A, float("nan"))
     pkg.sgemm_emu_stream_probe(A, B, C, threads=threads)
     assert torch.equal(C, A + B)
+
+
+def test_mfma_probe_computes_the_repeated_chunk_product():
+    """The products-only reference runs the full-tile kernel's products on
+    the first k chunk's fragments k / 32 times.  With small integers (hi
+    exact, lo zero) its output is exactly (k / 32) A[:, :32] @ B[:32, :];
+    the columns of A and rows of B it must not read hold NaN, and every
+    output is written.  With uniform inputs the correction products are
+    live: the error stays at the emulation's level (dropping lo would leave
+    errors near 2^-11 of the magnitudes)."""
+    dev = device()
+    g = torch.Generator().manual_seed(5)
+    m, n, k = 256, 512, 128
+    A = torch.full((m, 48), float("nan"))
+    B = torch.full((40, n), float("nan"))
+    A[:, :32] = torch.randint(-4, 5, (m, 32), generator=g).float()
+    B[:32, :] = torch.randint(-4, 5, (32, n), generator=g).float()
+    C = torch.full((m, n), float("nan"), device=dev)
+    pkg.sgemm_emu_mfma_probe(A.to(dev), B.to(dev), k, C)
+    want = (k // 32) * (A[:, :32].double() @ B[:32, :].double())
+    assert torch.equal(C.cpu().double(), want)
+
+    A = torch.rand((m, 32), generator=g) * 2 - 1
+    B = torch.rand((32, n), generator=g) * 2 - 1
+    C = pkg.sgemm_emu_mfma_probe(A.to(dev), B.to(dev), k)
+    exact = (k // 32) * (A.double() @ B.double())
+    norm = (k // 32) * (A.double().abs() @ B.double().abs())
+    err = ((C.cpu().double() - exact).abs() / norm).max().item()
+    assert err < 64 * 2.0**-23, err
+
