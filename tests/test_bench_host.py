@@ -73,3 +73,16 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_committed_traffic_describes_the_committed_kernels():
+    """Every counter run in profiles/traffic.json was taken on the kernel
+    sources as they stand, so the benchmark line can report its traffic; a
+    kernel or header change needs its counter runs taken again."""
+    with open(bench.TRAFFIC_FILE) as fh:
+        table = json.load(fh)
+    stale = [key for key, e in table.items()
+             if e["source_sha256"] != bench.kernel_source_hash(e["kernel"])]
+    assert not stale, f"counter runs older than their kernel sources: {stale}"
+    for key, e in table.items():
+        assert os.path.exists(os.path.join(ROOT, e["summary"])), key
