@@ -218,11 +218,19 @@ int sgemm_emu_resolve_policy(int m, int n, int k,
  *   column within a group).  tiles_m, tiles_n >= 1 and their product below
  *   2^31; each array holds tiles_m * tiles_n ints (caller-owned host
  *   memory).
- * Both return SGEMM_EMU_OK, SGEMM_EMU_ERR_DIM for sizes out of range, or
+ * sgemm_emu_block_order: the same for a launch of one item on the 128 x 256
+ *   full-tile kernel when tiles_m and tiles_n are multiples of 16 (e.g. the
+ *   8192 x 8192 product, 64 x 32 tiles): the 256 tasks the device runs at
+ *   once form one 16 x 16 block of tiles (each XCD an 8 x 4 part), blocks
+ *   taken down the columns, so that the XCDs share A rows and B columns in
+ *   the last-level cache.  SGEMM_EMU_ERR_DIM for grids that are not
+ *   multiples of 16 (those keep the grouped order).
+ * All three return SGEMM_EMU_OK, SGEMM_EMU_ERR_DIM for sizes out of range, or
  * SGEMM_EMU_ERR_NULL for a NULL array.
  */
 int sgemm_emu_xcd_order(int grid, int* task_of_workgroup);
 int sgemm_emu_tile_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col);
+int sgemm_emu_block_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col);
 
 /*
  * Batched multiply-accumulate in emulated FP32 with transposable operands:

@@ -24,8 +24,8 @@ __all__ = [
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
-    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
-    "sgemm_emu_mfma_probe",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_block_order",
+    "sgemm_emu_stream_probe", "sgemm_emu_mfma_probe",
     "HOUSEHOLDER_RULE", "HOUSEHOLDER_LDS", "SPLIT_SCALAR", "SPLIT_PAIR", "SPLIT_EIGHT",
     "OP_N", "OP_T", "ROW_MAJOR", "COL_MAJOR",
     "GIVENS_AUTO", "GIVENS_MAP", "GIVENS_EMBEDDED", "GIVENS_LDS",
@@ -55,8 +55,8 @@ EXPORTED_SYMBOLS = (
     "householder_emu_batched", "householder_emu_batched_ex", "givens_emu_batched",
     "sgemm_emu_split", "mfmae_num_elements", "mfmae_map", "mfmae_foreach", "mfmae_mma_probe",
     "sgemm_emu_strerror", "sgemm_emu_last_hip_error",
-    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_stream_probe",
-    "sgemm_emu_mfma_probe",
+    "sgemm_emu_xcd_order", "sgemm_emu_tile_order", "sgemm_emu_block_order",
+    "sgemm_emu_stream_probe", "sgemm_emu_mfma_probe",
 )
 
 
@@ -154,6 +154,7 @@ def load():
         "sgemm_emu_last_hip_error": ([], i32),
         "sgemm_emu_xcd_order": ([i32, P], i32),
         "sgemm_emu_tile_order": ([i32, i32, P, P], i32),
+        "sgemm_emu_block_order": ([i32, i32, P, P], i32),
         "sgemm_emu_stream_probe": ([i64, i64, P, P, P, i32, P], i32),
         "sgemm_emu_mfma_probe": ([i32, i32, i32, P, i32, P, i32, P, i32, P], i32),
     }
@@ -331,6 +332,23 @@ def sgemm_emu_tile_order(tiles_m: int, tiles_n: int):
                                        rows.ctypes.data_as(ctypes.c_void_p),
                                        cols.ctypes.data_as(ctypes.c_void_p)),
            "sgemm_emu_tile_order")
+    return rows, cols
+
+
+def sgemm_emu_block_order(tiles_m: int, tiles_n: int):
+    """(tile row, tile column) of each task of a one-item launch on the
+    128 x 256 full-tile kernel when both tile counts are multiples of 16 (the
+    device-wide block order, computed on the host): two numpy int32 arrays
+    of ``tiles_m * tiles_n`` entries."""
+    import numpy as np
+
+    count = max(int(tiles_m), 0) * max(int(tiles_n), 0)
+    rows = np.empty(count, dtype=np.int32)
+    cols = np.empty(count, dtype=np.int32)
+    _check(load().sgemm_emu_block_order(int(tiles_m), int(tiles_n),
+                                        rows.ctypes.data_as(ctypes.c_void_p),
+                                        cols.ctypes.data_as(ctypes.c_void_p)),
+           "sgemm_emu_block_order")
     return rows, cols
 
 

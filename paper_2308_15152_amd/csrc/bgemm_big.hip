@@ -459,7 +459,11 @@ __global__ __launch_bounds__(CF::NT, CF::W) void bgemm_big_kernel(BigParams p) {
     if (task >= p.ntasks) return;  // the whole workgroup leaves together
     const int tiles = p.tiles_m * p.tiles_n;
     const int item = task / tiles;
-    const TileRC rc = grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
+    // one large product on the 128 x 256 tile: tiles in device-wide blocks
+    const TileRC rc =
+        CF::BM == 128 && CF::BN == 256 && block_order_applies(p.tiles_m, p.tiles_n, p.ntasks)
+            ? block_tile(task - item * tiles, p.tiles_m, p.tiles_n)
+            : grouped_tile(task - item * tiles, p.tiles_m, p.tiles_n);
     const int m0 = rc.tm * CF::BM;
     const int n0 = rc.tn * CF::BN;
 

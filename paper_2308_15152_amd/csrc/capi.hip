@@ -437,6 +437,20 @@ int sgemm_emu_tile_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col)
     return SGEMM_EMU_OK;
 }
 
+int sgemm_emu_block_order(int tiles_m, int tiles_n, int* tile_row, int* tile_col) {
+    if (tiles_m < 1 || tiles_n < 1 || (int64_t)tiles_m * tiles_n > INT32_MAX ||
+        !sgemm_emu::block_order_applies(tiles_m, tiles_n, tiles_m * tiles_n))
+        return SGEMM_EMU_ERR_DIM;
+    if (tile_row == nullptr || tile_col == nullptr) return SGEMM_EMU_ERR_NULL;
+    const int tiles = tiles_m * tiles_n;
+    for (int t = 0; t < tiles; ++t) {
+        const sgemm_emu::TileRC rc = sgemm_emu::block_tile(t, tiles_m, tiles_n);
+        tile_row[t] = rc.tm;
+        tile_col[t] = rc.tn;
+    }
+    return SGEMM_EMU_OK;
+}
+
 int sgemm_emu_batched_acc(int op_a, int op_b, int layout_cd, int m, int n, int k, const float* A,
                           int lda, const float* B, int ldb, const float* C, int ldc, float* D,
                           int ldd, int batch, sgemm_emu_stride4_t stride, int shape, int ec,

@@ -74,6 +74,28 @@ __host__ __device__ inline TileRC grouped_tile(int t, int tiles_m, int tiles_n) 
     return {first_m + r % gm, r / gm};
 }
 
+// Tile order for one large product on the 128 x 256 tile (one item per
+// launch, tiles_m and tiles_n multiples of 16): the 256 tasks the device
+// runs at the same time -- 32 on each of the 8 XCDs, one workgroup per CU --
+// form one 16 x 16 block of tiles, each XCD an 8 x 4 part of it, so that the
+// XCDs share A rows (four each) and B columns (two each) in the last-level
+// cache, not only within their own L2.  Task t of XCD x = t / (G / 8) (the
+// numbering of xcd_task) is the s-th of that XCD, s = t mod (G / 8); block
+// s / 32, taken down the columns of blocks, position s mod 32 in the XCD's
+// part.  A bijection of [0, tiles_m tiles_n) onto the tile grid.
+__host__ __device__ inline bool block_order_applies(int tiles_m, int tiles_n, int ntasks) {
+    return tiles_m % 16 == 0 && tiles_n % 16 == 0 && (int64_t)tiles_m * tiles_n == ntasks;
+}
+
+__host__ __device__ inline TileRC block_tile(int t, int tiles_m, int tiles_n) {
+    const int per_xcd = tiles_m * tiles_n / 8;  // a multiple of 32
+    const int x = t / per_xcd, s = t - x * per_xcd;
+    const int w = s >> 5, i = s & 31;
+    const int blocks_m = tiles_m / 16;
+    const int bm = w % blocks_m, bn = w / blocks_m;
+    return {16 * bm + 8 * (x & 1) + (i & 7), 16 * bn + 4 * (x >> 1) + (i >> 3)};
+}
+
 // The persistent kernels: workgroup b of G walks tasks xcd_task(b, G) + i G.
 __device__ inline int first_task(const KParams& p) { return xcd_task(blockIdx.x, gridDim.x); }
 

@@ -138,7 +138,11 @@ struct MfmaProbeParams {
 
 __global__ __launch_bounds__(512, 2) void mfma_probe_kernel(MfmaProbeParams p) {
     using mfmae::half8_t;
-    const TileRC rc = grouped_tile(xcd_task(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n);
+    const int task = xcd_task(blockIdx.x, gridDim.x);
+    const int tiles = p.tiles_m * p.tiles_n;  // the grid: one task per tile
+    const TileRC rc = block_order_applies(p.tiles_m, p.tiles_n, tiles)
+                          ? block_tile(task, p.tiles_m, p.tiles_n)
+                          : grouped_tile(task, p.tiles_m, p.tiles_n);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int l = threadIdx.x & 63;
     const int g = l >> 5, j = l & 31;

@@ -158,6 +158,28 @@ def test_full_tile_kernel_shapes(flow, tile, shape):
     gate(to_np(Cd), ref, k, f"full-tile {tile} {shape}")
 
 
+@pytest.mark.parametrize("shape", [(2048, 4096, 64), (4096, 4096, 32), (2048, 8192, 32)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_full_tile_kernel_in_device_blocks(shape):
+    """One product on the 128 x 256 tile whose tile grid is a multiple of
+    16 x 16: the kernel takes its tiles in device-wide 16 x 16 blocks (one,
+    two and four blocks here, down the columns and across). Every output,
+    prefilled with NaN, against the oracle."""
+    m, n, k = shape
+    dev = device()
+    policy = pkg.Policy(pkg.FLOW_SPLIT, 1, pkg.TILE_128x256)
+    print(f"case device blocks {shape}", flush=True)
+    A, B = synth.gemm_inputs(1, m, n, k, seed=71 + m // 1024 + n // 1024)
+    Ad, Bd = A.to(dev), B.to(dev)
+    Cd = torch.full((1, m, n), float("nan"), device=dev)
+    _, kern = pkg.sgemm_emu_resolve_policy(Ad, Bd, Cd, policy=policy)
+    assert kern == "bgemm_big_kernel"
+    pkg.sgemm_emu_batched(Ad, Bd, Cd, policy=policy)
+    C = to_np(Cd)
+    assert np.isfinite(C).all()
+    gate(C, oracle.gemm(A.numpy(), B.numpy()), k, f"device blocks {shape}")
+
+
 LIMIT_CASES = [(pkg.FLOW_SPLIT, pkg.TILE_128x128, 128, 128),
                (pkg.FLOW_SPLIT, pkg.TILE_256x128, 256, 128),
                (pkg.FLOW_SPLIT, pkg.TILE_128x256, 128, 256),

@@ -85,6 +85,44 @@ def test_tile_order_groups_of_eight_rows():
         assert t == tm * tn
 
 
+def test_block_order_is_a_bijection():
+    for tm in range(16, 129, 16):
+        for tn in range(16, 129, 16):
+            r, c = pkg.sgemm_emu_block_order(tm, tn)
+            assert r.min() >= 0 and r.max() < tm and c.min() >= 0 and c.max() < tn
+            flat = r.astype(np.int64) * tn + c
+            assert np.array_equal(np.sort(flat), np.arange(tm * tn)), (tm, tn)
+
+
+def test_block_order_runs_one_block_of_tiles_at_a_time():
+    """With one workgroup per task dispatched round-robin over the 8 XCDs,
+    the 256 workgroups b in [256 w, 256 w + 256) (32 per XCD, one per CU)
+    take the tiles of one 16 x 16 block, blocks down the columns first, and
+    each XCD an 8 x 4 part of it: rows 8 (x mod 2) .. + 8, columns
+    4 (x div 2) .. + 4 of the block."""
+    for tm, tn in [(64, 32), (16, 16), (32, 48), (128, 16)]:
+        G = tm * tn
+        task = pkg.sgemm_emu_xcd_order(G)
+        r, c = pkg.sgemm_emu_block_order(tm, tn)
+        for w in range(G // 256):
+            bm, bn = w % (tm // 16), w // (tm // 16)
+            b = np.arange(256 * w, 256 * w + 256)
+            rows, cols = r[task[b]], c[task[b]]
+            assert set(zip(rows.tolist(), cols.tolist())) == {
+                (16 * bm + i, 16 * bn + j) for i in range(16) for j in range(16)}, (tm, tn, w)
+            x = b % 8
+            assert ((rows - 16 * bm) // 8 == x % 2).all()
+            assert ((cols - 16 * bn) // 4 == x // 2).all()
+
+
+def test_block_order_only_for_grids_of_whole_blocks():
+    lib = pkg.load()
+    buf = (ctypes.c_int * 4)()
+    for tm, tn in [(64, 33), (8, 16), (16, 8), (0, 16), (24, 32)]:
+        assert lib.sgemm_emu_block_order(tm, tn, buf, buf) == -1, (tm, tn)
+    assert lib.sgemm_emu_block_order(16, 16, None, buf) == -3
+
+
 def test_task_to_item_and_tile_covers_a_launch():
     """A launch of `items` items: task // tiles is the item and the grouped
     order of task % tiles the tile; with the XCD numbering over a grid of one
